@@ -1,0 +1,111 @@
+// Shared device helpers of the RingAda HIP kernels (gfx950 only).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rg {
+
+typedef uint16_t bf16;  // bfloat16 bit pattern
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ float bf2f(bf16 b) { return __uint_as_float((uint32_t)b << 16); }
+
+// round to nearest even; NaN stays NaN
+__device__ __forceinline__ bf16 f2bf(float f) {
+  uint32_t u = __float_as_uint(f);
+  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40);
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return (bf16)(u >> 16);
+}
+
+// storage abstraction: float or bf16 storage, fp32 arithmetic
+template <typename T> struct St;
+template <> struct St<float> {
+  static __device__ __forceinline__ float ld(const float* p, long i) { return p[i]; }
+  static __device__ __forceinline__ void st(float* p, long i, float v) { p[i] = v; }
+  // four consecutive elements (16 B aligned)
+  static __device__ __forceinline__ void ld4(const float* p, long i, float v[4]) {
+    float4 q = *reinterpret_cast<const float4*>(p + i);
+    v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
+  }
+  static __device__ __forceinline__ void st4(float* p, long i, const float v[4]) {
+    *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
+  }
+};
+template <> struct St<bf16> {
+  static __device__ __forceinline__ float ld(const bf16* p, long i) { return bf2f(p[i]); }
+  static __device__ __forceinline__ void st(bf16* p, long i, float v) { p[i] = f2bf(v); }
+  // four consecutive elements (8 B aligned)
+  static __device__ __forceinline__ void ld4(const bf16* p, long i, float v[4]) {
+    uint2 q = *reinterpret_cast<const uint2*>(p + i);
+    v[0] = __uint_as_float(q.x << 16); v[1] = __uint_as_float(q.x & 0xffff0000u);
+    v[2] = __uint_as_float(q.y << 16); v[3] = __uint_as_float(q.y & 0xffff0000u);
+  }
+  static __device__ __forceinline__ void st4(bf16* p, long i, const float v[4]) {
+    uint2 q;
+    q.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+    q.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    *reinterpret_cast<uint2*>(p + i) = q;
+  }
+};
+
+// ---------------------------------------------------------------- math
+__device__ __forceinline__ float gelu_f(float u) {  // u * Phi(u), erf form
+  return 0.5f * u * (1.f + erff(u * 0.70710678118654752f));
+}
+__device__ __forceinline__ float gelu_grad_f(float u) {  // Phi(u) + u phi(u)
+  float cdf = 0.5f * (1.f + erff(u * 0.70710678118654752f));
+  return cdf + u * 0.39894228040143268f * __expf(-0.5f * u * u);
+}
+__device__ __forceinline__ float sigmoid_f(float u) { return 1.f / (1.f + __expf(-u)); }
+
+// ---------------------------------------------------------------- MFMA
+// D[32x32] += A[32x16] * B[16x32]; lane l supplies A[l%32][8*(l/32)+v] and
+// B[8*(l/32)+v][l%32]; D lane l holds D[8*(r/4)+4*(l/32)+r%4][l%32].
+__device__ __forceinline__ f32x16 mfma32(bf16x8 a, bf16x8 b, f32x16 c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+}
+// D[16x16] += A[16x32] * B[32x16]; lane l supplies A[l%16][8*(l/16)+v] and
+// B[8*(l/16)+v][l%16]; D lane l holds D[4*(l/16)+r][l%16].
+__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
+}
+
+__device__ __forceinline__ bf16x8 ld_frag(const bf16* p) {  // 16 B
+  return *reinterpret_cast<const bf16x8*>(p);
+}
+__device__ __forceinline__ bf16x8 zero_frag() {
+  uint4 z = make_uint4(0, 0, 0, 0);
+  return __builtin_bit_cast(bf16x8, z);
+}
+__device__ __forceinline__ bf16x8 pack_frag(const float v[8]) {
+  uint4 q;
+  q.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
+  q.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+  q.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
+  q.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+  return __builtin_bit_cast(bf16x8, q);
+}
+__device__ __forceinline__ void unpack_frag(bf16x8 f, float v[8]) {
+  uint4 q = __builtin_bit_cast(uint4, f);
+  v[0] = __uint_as_float(q.x << 16); v[1] = __uint_as_float(q.x & 0xffff0000u);
+  v[2] = __uint_as_float(q.y << 16); v[3] = __uint_as_float(q.y & 0xffff0000u);
+  v[4] = __uint_as_float(q.z << 16); v[5] = __uint_as_float(q.z & 0xffff0000u);
+  v[6] = __uint_as_float(q.w << 16); v[7] = __uint_as_float(q.w & 0xffff0000u);
+}
+
+// ---------------------------------------------------------------- reductions
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+}  // namespace rg

@@ -1,0 +1,560 @@
+// Bottleneck adapters of Eq. (1), h <- h + gelu(h W_down) W_up, fused with the
+// residual add and the normalisation that follow them in the block, and their
+// backward with the fp32 weight-gradient accumulation.
+//
+// bf16 row kernels: one workgroup per 16 tokens.  Both adapter contractions
+// use MFMA 16x16x32 in the transposed orientation (the weight is the A operand,
+// the 16 tokens the B operand), so every lane ends up owning four consecutive
+// features of one token; row statistics of the norm reduce over the four
+// lanes sharing a token (shuffles) and then over waves (LDS).
+// Weight gradients are long-K (K = tokens), tiny-output contractions: a
+// split-K MFMA kernel with LDS-transposed tiles and fp32 atomics.
+#include "common.h"
+#include "kernels.h"
+
+namespace rg {
+
+constexpr int TOK = 16;   // tokens per workgroup of the bf16 row kernels
+constexpr int MB = 64;    // adapter bottleneck of the bf16 path
+constexpr int GP = MB + 8;
+
+// ================================================================ bf16 forward
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
+  constexpr int KS = NW / 4;  // k-splits of the down projection
+  __shared__ __attribute__((aligned(16))) bf16 sG[TOK * GP];
+  __shared__ float sUp[KS > 1 ? KS : 1][TOK][MB];
+  __shared__ float sRed[NW][TOK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int d = a.d, T = a.T;
+  const int token = blockIdx.x * TOK + l16;
+  const bool tv = token < T;
+  const long trow = (long)(tv ? token : 0) * d;
+  const bf16* z = static_cast<const bf16*>(a.z);
+
+  // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:]
+  {
+    const int ug = wave % 4, ks = wave / 4, slice = d / KS;
+    const bf16* wd = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * d + 8 * grp;
+    const bf16* zr = z + trow + 8 * grp;
+    f32x4 u = {0.f, 0.f, 0.f, 0.f};
+    for (int kk = ks * slice; kk < (ks + 1) * slice; kk += 32)
+      u = mfma16(ld_frag(wd + kk), tv ? ld_frag(zr + kk) : zero_frag(), u);
+    if constexpr (KS > 1) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sUp[ks][l16][ug * 16 + 4 * grp + r] = u[r];
+      __syncthreads();
+      if (ks == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float s = 0.f;
+#pragma unroll
+          for (int k2 = 0; k2 < KS; ++k2) s += sUp[k2][l16][ug * 16 + 4 * grp + r];
+          u[r] = s;
+        }
+      }
+    }
+    if (ks == 0) {
+      float uv[4] = {u[0], u[1], u[2], u[3]};
+      if (a.u && tv) St<bf16>::st4(static_cast<bf16*>(a.u), (long)token * MB + ug * 16 + 4 * grp, uv);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sG[l16 * GP + ug * 16 + 4 * grp + r] = f2bf(gelu_f(uv[r]));
+    }
+  }
+  __syncthreads();
+
+  // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  + z + res
+  const int FW = d / NW, FB = FW / 16, f0 = wave * FW;
+  float v[16][4];
+  {
+    const bf16* wu = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
+    const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+#pragma unroll
+    for (int b = 0; b < 16; ++b) {
+      if (b < FB) {
+        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+        acc = mfma16(ld_frag(wu + (long)b * 16 * MB), g0, acc);
+        acc = mfma16(ld_frag(wu + (long)b * 16 * MB + 32), g1, acc);
+        const int f = f0 + b * 16 + 4 * grp;
+        float zz[4], rr[4];
+        if (tv) {
+          St<bf16>::ld4(z, trow + f, zz);
+          St<bf16>::ld4(static_cast<const bf16*>(a.res), trow + f, rr);
+        } else {
+#pragma unroll
+          for (int q = 0; q < 4; ++q) zz[q] = rr[q] = 0.f;
+        }
+#pragma unroll
+        for (int q = 0; q < 4; ++q) v[b][q] = acc[q] + zz[q] + rr[q];
+      }
+    }
+  }
+
+  auto row_sum = [&](float s) {  // sum over the token's features across the workgroup
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    if (grp == 0) sRed[wave][l16] = s;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) t += sRed[w][l16];
+    __syncthreads();
+    return t;
+  };
+
+  if (a.norm == Norm::None) {
+    if (tv)
+#pragma unroll
+      for (int b = 0; b < 16; ++b)
+        if (b < FB) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
+    return;
+  }
+  const float inv_d = 1.f / (float)d;
+  float mean = 0.f;
+  if (a.norm == Norm::LN) {
+    float s = 0.f;
+#pragma unroll
+    for (int b = 0; b < 16; ++b)
+      if (b < FB)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) s += v[b][q];
+    mean = row_sum(s) * inv_d;
+  } else if (tv) {
+#pragma unroll
+    for (int b = 0; b < 16; ++b)  // RMS: the residual stream h itself is an output
+      if (b < FB) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
+  }
+  float s2 = 0.f;
+#pragma unroll
+  for (int b = 0; b < 16; ++b)
+    if (b < FB)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float c = v[b][q] - mean;
+        s2 += c * c;
+      }
+  const float rstd = rsqrtf(row_sum(s2) * inv_d + a.eps);
+  if (!tv) return;
+  if (a.rstd && wave == 0 && grp == 0) a.rstd[token] = rstd;
+  bf16* out = static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm);
+#pragma unroll
+  for (int b = 0; b < 16; ++b) {
+    if (b < FB) {
+      const int f = f0 + b * 16 + 4 * grp;
+      float xh[4], gm[4], bt[4], o[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) xh[q] = (v[b][q] - mean) * rstd;
+      St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
+      if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
+      else
+#pragma unroll
+        for (int q = 0; q < 4; ++q) bt[q] = 0.f;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
+      St<bf16>::st4(out, trow + f, o);
+      if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), trow + f, xh);
+    }
+  }
+}
+
+// ================================================================ bf16 backward
+template <int NW>
+__global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
+  constexpr int KS = NW / 4;
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  const int d = a.d, T = a.T, DP = d + 8;
+  bf16* sdZ = reinterpret_cast<bf16*>(smem);                       // [TOK][d + 8]
+  bf16* sdU = sdZ + TOK * DP;                                      // [TOK][GP]
+  float* sPart = reinterpret_cast<float*>(sdU + TOK * GP);         // [KS][TOK][MB]
+  float* sRed = sPart + KS * TOK * MB;                             // [NW][TOK]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int token = blockIdx.x * TOK + l16;
+  const bool tv = token < T;
+  const long trow = (long)(tv ? token : 0) * d;
+  const int FW = d / NW, FB = FW / 16, f0 = wave * FW;
+
+  auto row_sum = [&](float s) {
+    s += __shfl_xor(s, 16, 64);
+    s += __shfl_xor(s, 32, 64);
+    if (grp == 0) sRed[wave * TOK + l16] = s;
+    __syncthreads();
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) t += sRed[w * TOK + l16];
+    __syncthreads();
+    return t;
+  };
+
+  // ---- gradient at the adapter output
+  float dz[16][4];
+  {
+    float gg[16][4], xh[16][4];
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int b = 0; b < 16; ++b) {
+      if (b < FB) {
+        const int f = f0 + b * 16 + 4 * grp;
+        if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.gin), trow + f, gg[b]);
+        else
+#pragma unroll
+          for (int q = 0; q < 4; ++q) gg[b][q] = 0.f;
+        if (a.norm != Norm::None) {
+          float gm[4];
+          St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
+          if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), trow + f, xh[b]);
+          else
+#pragma unroll
+            for (int q = 0; q < 4; ++q) xh[b][q] = 0.f;
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            gg[b][q] *= gm[q];
+            s1 += gg[b][q];
+            s2 += gg[b][q] * xh[b][q];
+          }
+        }
+      }
+    }
+    if (a.norm == Norm::None) {
+#pragma unroll
+      for (int b = 0; b < 16; ++b)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dz[b][q] = gg[b][q];
+    } else {
+      const float inv_d = 1.f / (float)d;
+      const float m1 = (a.norm == Norm::LN) ? row_sum(s1) * inv_d : 0.f;
+      const float m2 = row_sum(s2) * inv_d;
+      const float rs = tv ? a.rstd[token] : 0.f;
+#pragma unroll
+      for (int b = 0; b < 16; ++b) {
+        if (b < FB) {
+          float dr[4] = {0.f, 0.f, 0.f, 0.f};
+          if (a.norm == Norm::RMS && tv)
+            St<bf16>::ld4(static_cast<const bf16*>(a.dres), trow + f0 + b * 16 + 4 * grp, dr);
+#pragma unroll
+          for (int q = 0; q < 4; ++q) dz[b][q] = dr[q] + rs * (gg[b][q] - m1 - xh[b][q] * m2);
+        }
+      }
+    }
+  }
+#pragma unroll
+  for (int b = 0; b < 16; ++b) {
+    if (b < FB) {
+      const int f = f0 + b * 16 + 4 * grp;
+      if (tv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), trow + f, dz[b]);
+      St<bf16>::st4(sdZ, (long)l16 * DP + f, dz[b]);
+    }
+  }
+  __syncthreads();
+
+  // ---- dV^T[unit][token] = W_up[unit][:] . dZ[token][:]; dU = dV * gelu'(U)
+  {
+    const int ug = wave % 4, ks = wave / 4, slice = d / KS;
+    const bf16* wu = static_cast<const bf16*>(a.wup) + (long)(ug * 16 + l16) * d + 8 * grp;
+    const bf16* zr = sdZ + l16 * DP + 8 * grp;
+    f32x4 dv = {0.f, 0.f, 0.f, 0.f};
+    for (int kk = ks * slice; kk < (ks + 1) * slice; kk += 32) dv = mfma16(ld_frag(wu + kk), ld_frag(zr + kk), dv);
+    if constexpr (KS > 1) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) sPart[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = dv[r];
+      __syncthreads();
+      if (ks == 0) {
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          float s = 0.f;
+#pragma unroll
+          for (int k2 = 0; k2 < KS; ++k2) s += sPart[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
+          dv[r] = s;
+        }
+      }
+    }
+    if (ks == 0) {
+      const int j0 = ug * 16 + 4 * grp;
+      float uu[4] = {0.f, 0.f, 0.f, 0.f}, du[4];
+      if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.u), (long)token * MB + j0, uu);
+#pragma unroll
+      for (int r = 0; r < 4; ++r) du[r] = dv[r] * gelu_grad_f(uu[r]);
+      if (tv) St<bf16>::st4(static_cast<bf16*>(a.du), (long)token * MB + j0, du);
+      St<bf16>::st4(sdU, (long)l16 * GP + j0, du);
+    }
+  }
+  if (!a.dzin) return;
+  __syncthreads();
+
+  // ---- dzin^T[f][token] = dZ + W_down[f][:] . dU[token][:]
+  const bf16* wd = static_cast<const bf16*>(a.wdn) + (long)(f0 + l16) * MB + 8 * grp;
+  const bf16x8 u0 = ld_frag(sdU + l16 * GP + 8 * grp), u1 = ld_frag(sdU + l16 * GP + 32 + 8 * grp);
+#pragma unroll
+  for (int b = 0; b < 16; ++b) {
+    if (b < FB) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mfma16(ld_frag(wd + (long)b * 16 * MB), u0, acc);
+      acc = mfma16(ld_frag(wd + (long)b * 16 * MB + 32), u1, acc);
+      float o[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) o[q] = dz[b][q] + acc[q];
+      if (tv) St<bf16>::st4(static_cast<bf16*>(a.dzin), trow + f0 + b * 16 + 4 * grp, o);
+    }
+  }
+}
+
+// ================================================================ bf16 weight gradients
+// C[p][q] += sum_t X[t][p] * Y[t][q]: blockIdx.z = 0 -> dW_up (X = gelu(U), Y = dZ),
+// 1 -> dW_down (X = z, Y = dU).  64x64 output tiles, 256 tokens per workgroup.
+constexpr int DW_TC = 256;
+__global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [p][token]
+  __shared__ __attribute__((aligned(16))) bf16 sY[64 * GP];  // [q][token]
+  const bool up = blockIdx.z == 0;
+  const int d = a.d, T = a.T;
+  const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
+  const bf16* Y = static_cast<const bf16*>(up ? a.dz : a.du);
+  const int ldx = up ? MB : d, ldy = up ? d : MB;
+  float* C = up ? a.g_up : a.g_down;
+  const int ldc = up ? d : MB;
+  const int p0 = up ? 0 : blockIdx.x * 64, q0 = up ? blockIdx.x * 64 : 0;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, half = lane >> 5;
+  const int wp = wave / 2, wq = wave % 2;
+  f32x16 acc;
+#pragma unroll
+  for (int r = 0; r < 16; ++r) acc[r] = 0.f;
+  const int tbeg = blockIdx.y * DW_TC, tend = min(T, tbeg + DW_TC);
+  for (int t0 = tbeg; t0 < tend; t0 += 64) {
+    __syncthreads();
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {  // 64 tokens x 8 chunks of 8 columns, for X and Y
+      const int idx = tid + i * 256, tt = idx / 8, c = idx % 8, t = t0 + tt;
+      float xv[8], yv[8];
+      if (t < tend) {
+        unpack_frag(ld_frag(X + (long)t * ldx + p0 + c * 8), xv);
+        unpack_frag(ld_frag(Y + (long)t * ldy + q0 + c * 8), yv);
+        if (up)
+#pragma unroll
+          for (int v = 0; v < 8; ++v) xv[v] = gelu_f(xv[v]);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 8; ++v) xv[v] = yv[v] = 0.f;
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        sX[(c * 8 + v) * GP + tt] = f2bf(xv[v]);
+        sY[(c * 8 + v) * GP + tt] = f2bf(yv[v]);
+      }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int ks = 0; ks < 4; ++ks)
+      acc = mfma32(ld_frag(sX + (wp * 32 + l32) * GP + ks * 16 + 8 * half),
+                   ld_frag(sY + (wq * 32 + l32) * GP + ks * 16 + 8 * half), acc);
+  }
+  // D[i = p][j = q]: lane holds q = wq*32 + l32, p = wp*32 + 8*(r/4) + 4*half + r%4
+#pragma unroll
+  for (int r = 0; r < 16; ++r) {
+    const int p = p0 + wp * 32 + 8 * (r >> 2) + 4 * half + (r & 3), q = q0 + wq * 32 + l32;
+    unsafeAtomicAdd(C + (long)p * ldc + q, acc[r]);
+  }
+}
+
+// ================================================================ fp32 (small stages): one workgroup per token
+__device__ float block_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int w = 0; w < nw; ++w) t += red[w];
+  return t;
+}
+
+__global__ __launch_bounds__(256) void adapter_fwd_f32(AdapterFwdArgs a) {
+  extern __shared__ float sh[];
+  const int d = a.d, m = a.m, t = blockIdx.x;
+  float* sz = sh;        // [d]
+  float* sg = sz + d;    // [m]
+  float* sv = sg + m;    // [d]
+  float* red = sv + d;   // [8]
+  const float* z = static_cast<const float*>(a.z) + (long)t * d;
+  const float* res = static_cast<const float*>(a.res) + (long)t * d;
+  const float* wdt = static_cast<const float*>(a.wdn_t);
+  const float* wut = static_cast<const float*>(a.wup_t);
+  for (int i = threadIdx.x; i < d; i += blockDim.x) sz[i] = z[i];
+  __syncthreads();
+  for (int j = threadIdx.x; j < m; j += blockDim.x) {
+    float u = 0.f;
+    for (int k = 0; k < d; ++k) u += sz[k] * wdt[(long)j * d + k];
+    if (a.u) static_cast<float*>(a.u)[(long)t * m + j] = u;
+    sg[j] = gelu_f(u);
+  }
+  __syncthreads();
+  float s1 = 0.f;
+  for (int f = threadIdx.x; f < d; f += blockDim.x) {
+    float v = res[f] + sz[f];
+    for (int j = 0; j < m; ++j) v += sg[j] * wut[(long)f * m + j];
+    sv[f] = v;
+    s1 += v;
+  }
+  float* out = static_cast<float*>(a.out) + (long)t * d;
+  if (a.norm == Norm::None) {
+    for (int f = threadIdx.x; f < d; f += blockDim.x) out[f] = sv[f];
+    return;
+  }
+  float mean = 0.f;
+  if (a.norm == Norm::LN) mean = block_sum(s1, red) / d;
+  else
+    for (int f = threadIdx.x; f < d; f += blockDim.x) out[f] = sv[f];
+  float s2 = 0.f;
+  for (int f = threadIdx.x; f < d; f += blockDim.x) s2 += (sv[f] - mean) * (sv[f] - mean);
+  const float rstd = rsqrtf(block_sum(s2, red) / d + a.eps);
+  if (a.rstd && threadIdx.x == 0) a.rstd[t] = rstd;
+  float* o = (a.norm == Norm::LN) ? out : static_cast<float*>(a.out_norm) + (long)t * d;
+  const float* gm = static_cast<const float*>(a.gamma);
+  const float* bt = static_cast<const float*>(a.beta);
+  for (int f = threadIdx.x; f < d; f += blockDim.x) {
+    const float xh = (sv[f] - mean) * rstd;
+    o[f] = xh * gm[f] + (a.norm == Norm::LN ? bt[f] : 0.f);
+    if (a.xhat) static_cast<float*>(a.xhat)[(long)t * d + f] = xh;
+  }
+}
+
+__global__ __launch_bounds__(256) void adapter_bwd_f32(AdapterBwdArgs a) {
+  extern __shared__ float sh[];
+  const int d = a.d, m = a.m, t = blockIdx.x;
+  float* sdz = sh;       // [d]
+  float* sdu = sdz + d;  // [m]
+  float* red = sdu + m;  // [8]
+  const float* gin = static_cast<const float*>(a.gin) + (long)t * d;
+  const float* xh = static_cast<const float*>(a.xhat) + (long)t * d;
+  const float* gm = static_cast<const float*>(a.gamma);
+  if (a.norm == Norm::None) {
+    for (int f = threadIdx.x; f < d; f += blockDim.x) sdz[f] = gin[f];
+  } else {
+    float s1 = 0.f, s2 = 0.f;
+    for (int f = threadIdx.x; f < d; f += blockDim.x) {
+      const float g = gin[f] * gm[f];
+      s1 += g;
+      s2 += g * xh[f];
+    }
+    const float m1 = (a.norm == Norm::LN) ? block_sum(s1, red) / d : 0.f;
+    const float m2 = block_sum(s2, red) / d;
+    const float rs = a.rstd[t];
+    const float* dres = static_cast<const float*>(a.dres);
+    for (int f = threadIdx.x; f < d; f += blockDim.x) {
+      const float g = gin[f] * gm[f];
+      sdz[f] = (a.norm == Norm::RMS ? dres[(long)t * d + f] : 0.f) + rs * (g - m1 - xh[f] * m2);
+    }
+  }
+  __syncthreads();
+  if (a.dz) {
+    float* dzo = static_cast<float*>(a.dz) + (long)t * d;
+    for (int f = threadIdx.x; f < d; f += blockDim.x) dzo[f] = sdz[f];
+  }
+  const float* wu = static_cast<const float*>(a.wup);
+  const float* wd = static_cast<const float*>(a.wdn);
+  const float* u = static_cast<const float*>(a.u) + (long)t * m;
+  for (int j = threadIdx.x; j < m; j += blockDim.x) {
+    float dv = 0.f;
+    for (int f = 0; f < d; ++f) dv += sdz[f] * wu[(long)j * d + f];
+    const float du = dv * gelu_grad_f(u[j]);
+    sdu[j] = du;
+    static_cast<float*>(a.du)[(long)t * m + j] = du;
+  }
+  if (!a.dzin) return;
+  __syncthreads();
+  float* dzin = static_cast<float*>(a.dzin) + (long)t * d;
+  for (int f = threadIdx.x; f < d; f += blockDim.x) {
+    float v = sdz[f];
+    for (int j = 0; j < m; ++j) v += sdu[j] * wd[(long)f * m + j];
+    dzin[f] = v;
+  }
+}
+
+// one thread per gradient entry, summing over every token
+__global__ __launch_bounds__(256) void adapter_dw_f32(AdapterDwArgs a) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long n = (long)a.m * a.d;
+  if (i >= 2 * n) return;
+  const float* U = static_cast<const float*>(a.u);
+  const float* dZ = static_cast<const float*>(a.dz);
+  const float* Z = static_cast<const float*>(a.z);
+  const float* dU = static_cast<const float*>(a.du);
+  float s = 0.f;
+  if (i < n) {  // g_up[j][f]
+    const int j = (int)(i / a.d), f = (int)(i % a.d);
+    for (int t = 0; t < a.T; ++t) s += gelu_f(U[(long)t * a.m + j]) * dZ[(long)t * a.d + f];
+    a.g_up[i] += s;
+  } else {      // g_down[f][j]
+    const long k = i - n;
+    const int f = (int)(k / a.m), j = (int)(k % a.m);
+    for (int t = 0; t < a.T; ++t) s += Z[(long)t * a.d + f] * dU[(long)t * a.m + j];
+    a.g_down[k] += s;
+  }
+}
+
+// ================================================================ launchers
+static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+static int bf16_waves(int d) {  // waves per row-kernel workgroup, 0 if unsupported
+  if (d % 64 == 0 && d <= 1024) return 4;
+  if (d % 256 == 0 && d <= 4096) return 16;
+  return 0;
+}
+
+hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s) {
+  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.z || !a.res || !a.wdn_t || !a.wup_t || !a.out)
+    return hipErrorInvalidValue;
+  if (a.norm != Norm::None && !a.gamma) return hipErrorInvalidValue;
+  if (a.norm == Norm::LN && !a.beta) return hipErrorInvalidValue;
+  if (a.norm == Norm::RMS && !a.out_norm) return hipErrorInvalidValue;
+  if (a.T == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    const int nw = bf16_waves(a.d);
+    if (!nw || a.m != MB || !al16(a.z) || !al16(a.wdn_t) || !al16(a.wup_t)) return hipErrorInvalidValue;
+    const dim3 grid((a.T + TOK - 1) / TOK);
+    if (nw == 4) hipLaunchKernelGGL(adapter_fwd_bf16<4>, grid, dim3(256), 0, s, a);
+    else hipLaunchKernelGGL(adapter_fwd_bf16<16>, grid, dim3(1024), 0, s, a);
+    return hipGetLastError();
+  }
+  const size_t sh = (2 * (size_t)a.d + a.m + 8) * sizeof(float);
+  if (sh > 64 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adapter_fwd_f32, dim3(a.T), dim3(256), sh, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s) {
+  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.gin || !a.u || !a.wup || !a.wdn || !a.du)
+    return hipErrorInvalidValue;
+  if (!a.dz && a.norm != Norm::None) return hipErrorInvalidValue;
+  if (a.norm != Norm::None && (!a.xhat || !a.rstd || !a.gamma)) return hipErrorInvalidValue;
+  if (a.norm == Norm::RMS && !a.dres) return hipErrorInvalidValue;
+  if (a.T == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    const int nw = bf16_waves(a.d);
+    if (!nw || a.m != MB || !al16(a.wup) || !al16(a.wdn)) return hipErrorInvalidValue;
+    const size_t sh = (size_t)TOK * (a.d + 8) * 2 + (size_t)TOK * GP * 2 +
+                      (size_t)(nw / 4) * TOK * MB * 4 + (size_t)nw * TOK * 4;
+    const dim3 grid((a.T + TOK - 1) / TOK);
+    if (nw == 4) hipLaunchKernelGGL(adapter_bwd_bf16<4>, grid, dim3(256), sh, s, a);
+    else hipLaunchKernelGGL(adapter_bwd_bf16<16>, grid, dim3(1024), sh, s, a);
+    return hipGetLastError();
+  }
+  const size_t sh = ((size_t)a.d + a.m + 8) * sizeof(float);
+  if (sh > 64 * 1024) return hipErrorInvalidValue;
+  hipLaunchKernelGGL(adapter_bwd_f32, dim3(a.T), dim3(256), sh, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s) {
+  if (a.T < 0 || !a.u || !a.dz || !a.z || !a.du || !a.g_up || !a.g_down) return hipErrorInvalidValue;
+  if (a.T == 0) return hipSuccess;
+  if (dtype == DT_BF16) {
+    if (a.m != MB || a.d % 64) return hipErrorInvalidValue;
+    const dim3 grid(a.d / 64, (a.T + DW_TC - 1) / DW_TC, 2);
+    hipLaunchKernelGGL(adapter_dw_bf16, grid, dim3(256), 0, s, a);
+    return hipGetLastError();
+  }
+  const long n = 2L * a.m * a.d;
+  hipLaunchKernelGGL(adapter_dw_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace rg

@@ -1,0 +1,582 @@
+// Attention core of the frozen blocks: softmax(Q K^T / sqrt(d_head) [+causal]) V
+// per (batch, head), and its backward (dQ, dK, dV; frozen projections around it
+// are plain GEMMs).  Rotary embedding (rotate-half pairs (i, i + d_head/2)) is
+// applied to Q and K as they are loaded, so the stash keeps the pre-rotation
+// projections and the backward rotates the gradients back.
+//
+// bf16 kernels use MFMA 32x32x16 with K/V (or Q/dO) tiles staged in LDS.
+// Each wave owns 32 queries (forward, dQ pass) or 32 keys (dK/dV pass), so the
+// score block held in registers has a fixed query (key) per lane and the
+// softmax row statistics are mostly in-lane.  The probabilities are fed back
+// to the second MFMA straight from registers: within one 16-wide k step the
+// lane's values cover 16 keys in a fixed permuted order, and the other operand
+// is read from a transposed LDS tile in that same order.
+//
+// Log-sum-exp is kept in base 2 of the scaled scores: lse2 = log2 sum_j
+// 2^(s_j * scale * log2 e).
+#include "common.h"
+#include "kernels.h"
+
+namespace rg {
+
+constexpr float kLog2e = 1.4426950408889634f;
+
+__device__ __forceinline__ void rope_cs(int pos, int i, int dh, float log2theta, float* c, float* s) {
+  const float inv_freq = exp2f(-(2.f * (float)i / (float)dh) * log2theta);
+  sincosf((float)pos * inv_freq, s, c);
+}
+
+// ================================================================ bf16 / MFMA
+constexpr int KT = 64;       // keys (or queries) per LDS tile
+constexpr int TP = KT + 8;   // pitch of transposed tiles [dim][KT]
+
+// Loads a [KT x DH] tile of rows r0.. (rows >= S are zero) from the Q/K/V
+// column block `col` into LDS row-major (pitch DH + 8) and/or transposed
+// (pitch TP), rotating pairs (i, i + DH/2) when rot.
+template <int DH>
+__device__ __forceinline__ void load_tile(const bf16* qkv, int ld, int b, int S, int r0, int col,
+                                          bool rot, float log2theta, bf16* rowmaj, bf16* trans) {
+  constexpr int HC = DH / 16;  // 8-element chunk pairs per row (chunk c with c + DH/16)
+  constexpr int PAIRS = KT * HC;
+  for (int p = threadIdx.x; p < PAIRS; p += blockDim.x) {
+    const int r = p / HC, c = p % HC, row = r0 + r;
+    float x1[8], x2[8];
+    if (row < S) {
+      const bf16* src = qkv + (long)(b * S + row) * ld + col;
+      unpack_frag(ld_frag(src + c * 8), x1);
+      unpack_frag(ld_frag(src + c * 8 + DH / 2), x2);
+      if (rot) {
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          float cs, sn;
+          rope_cs(row, c * 8 + v, DH, log2theta, &cs, &sn);
+          const float a = x1[v], bb = x2[v];
+          x1[v] = a * cs - bb * sn;
+          x2[v] = bb * cs + a * sn;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int v = 0; v < 8; ++v) x1[v] = x2[v] = 0.f;
+    }
+    if (rowmaj) {
+      *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8) = pack_frag(x1);
+      *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8 + DH / 2) = pack_frag(x2);
+    }
+    if (trans) {
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        trans[(c * 8 + v) * TP + r] = f2bf(x1[v]);
+        trans[(c * 8 + DH / 2 + v) * TP + r] = f2bf(x2[v]);
+      }
+    }
+  }
+}
+
+// Fragments (B operand, k = head dim) of one row held by this lane: dims
+// 16s + 8*(lane/32) + v, rotated when rot.
+template <int DH>
+__device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool valid, bool rot,
+                                               float log2theta, int half, bf16x8 f[DH / 16]) {
+  float x[DH / 16][8];
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) {
+    if (valid) unpack_frag(ld_frag(src + 16 * s + 8 * half), x[s]);
+    else
+#pragma unroll
+      for (int v = 0; v < 8; ++v) x[s][v] = 0.f;
+  }
+  if (rot && valid) {
+#pragma unroll
+    for (int s = 0; s < DH / 32; ++s)
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        float cs, sn;
+        rope_cs(pos, 16 * s + 8 * half + v, DH, log2theta, &cs, &sn);
+        const float a = x[s][v], bb = x[s + DH / 32][v];
+        x[s][v] = a * cs - bb * sn;
+        x[s + DH / 32][v] = bb * cs + a * sn;
+      }
+  }
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) f[s] = pack_frag(x[s]);
+}
+
+// A-operand fragment from a transposed tile: row `dimrow`, the 8 permuted
+// positions matching register values r = 8j..8j+7 of score block kb.
+__device__ __forceinline__ bf16x8 perm_frag(const bf16* trans, int dimrow, int kb, int j, int half) {
+  const bf16* p = trans + dimrow * TP + kb * 32 + 16 * j + 4 * half;
+  uint2 lo = *reinterpret_cast<const uint2*>(p);
+  uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
+  uint4 q = make_uint4(lo.x, lo.y, hi.x, hi.y);
+  return __builtin_bit_cast(bf16x8, q);
+}
+
+__device__ __forceinline__ bf16x8 pack8(const f32x16& v, int j) {
+  float t[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) t[i] = v[8 * j + i];
+  return pack_frag(t);
+}
+
+// position of register value r within a 32-wide score block for this lane half
+__device__ __forceinline__ int perm_pos(int r, int half) { return 8 * (r >> 2) + 4 * half + (r & 3); }
+
+// Writes a 32-row x DH accumulator (transposed layout: lane = row, dims
+// 8*(r/4) + 4*half + r%4 of block db) scaled, optionally un-rotated.
+template <int DH>
+__device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, bool unrot, int pos,
+                                           float log2theta, int half, bf16* dst) {
+  if (unrot) {
+#pragma unroll
+    for (int db = 0; db < DH / 64; ++db)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int i = db * 32 + perm_pos(r, half);
+        float cs, sn;
+        rope_cs(pos, i, DH, log2theta, &cs, &sn);
+        const float d1 = acc[db][r], d2 = acc[db + DH / 64][r];
+        acc[db][r] = d1 * cs + d2 * sn;
+        acc[db + DH / 64][r] = d2 * cs - d1 * sn;
+      }
+  }
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = acc[db][4 * g + q] * scale;
+      St<bf16>::st4(dst, db * 32 + 8 * g + 4 * half, v);
+    }
+}
+
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sVt[DH * TP];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int q = blockIdx.x * 128 + wave * 32 + l32;
+  const bool qv = q < S;
+  const int d = a.H * DH;
+  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float sl2 = kLog2e * rsqrtf((float)DH);
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+
+  bf16x8 qf[DH / 16];
+  load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * DH, q, qv, a.rope,
+                     log2theta, half, qf);
+
+  f32x16 oacc[DH / 32];
+#pragma unroll
+  for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
+  float mrun = -INFINITY, lrun = 0.f;
+
+  const int qlast = min(S - 1, blockIdx.x * 128 + 127);
+  const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
+  for (int kt = 0; kt < nkt; ++kt) {
+    __syncthreads();
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK, nullptr);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, nullptr, sVt);
+    __syncthreads();
+    f32x16 sc[2];
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sc[kb][r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < DH / 16; ++s)
+        sc[kb] = mfma32(ld_frag(sK + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), qf[s], sc[kb]);
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt * KT + kb * 32 + perm_pos(r, half);
+        const bool ok = key < S && (!CAUSAL || key <= q);
+        sc[kb][r] = ok ? sc[kb][r] * sl2 : -INFINITY;
+        mx = fmaxf(mx, sc[kb][r]);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
+    const float mnew = fmaxf(mrun, mx);
+    const float alpha = exp2f(mrun - mnew);  // 0 on the first tile
+    float rs = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        sc[kb][r] = exp2f(sc[kb][r] - mnew);
+        rs += sc[kb][r];
+      }
+    rs += __shfl_xor(rs, 32, 64);
+    lrun = lrun * alpha + rs;
+    mrun = mnew;
+#pragma unroll
+    for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 pf = pack8(sc[kb], j);
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db)
+          oacc[db] = mfma32(perm_frag(sVt, db * 32 + l32, kb, j, half), pf, oacc[db]);
+      }
+  }
+  if (qv) {
+    bf16* o = static_cast<bf16*>(a.o) + (long)(b * S + q) * a.ld_o + hd * DH;
+    store_rows<DH>(oacc, 1.f / lrun, false, q, 0.f, half, o);
+    if (half == 0) a.lse[(long)bh * S + q] = mrun + log2f(lrun);
+  }
+}
+
+// dQ pass (lane = query); also writes D = rowsum(dO * O)
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sKt[DH * TP];
+  __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int q = blockIdx.x * 128 + wave * 32 + l32;
+  const bool qv = q < S;
+  const int d = a.H * DH;
+  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+  const long qrow = (long)(b * S + (qv ? q : 0));
+
+  bf16x8 qf[DH / 16], df[DH / 16];
+  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * DH, q, qv, a.rope, log2theta, half, qf);
+  load_row_frags<DH>(static_cast<const bf16*>(a.dout) + qrow * a.ld_do + hd * DH, q, qv, false,
+                     0.f, half, df);
+  float dsum = 0.f;
+  {
+    const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      float ov[8], dv[8];
+      if (qv) unpack_frag(ld_frag(orow + 16 * s + 8 * half), ov);
+      else
+        for (int v = 0; v < 8; ++v) ov[v] = 0.f;
+      unpack_frag(df[s], dv);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
+    }
+    dsum += __shfl_xor(dsum, 32, 64);
+  }
+  const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
+  if (qv && half == 0) a.dsum[(long)bh * S + q] = dsum;
+
+  f32x16 dq[DH / 32];
+#pragma unroll
+  for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
+
+  const int qlast = min(S - 1, blockIdx.x * 128 + 127);
+  const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
+  for (int kt = 0; kt < nkt; ++kt) {
+    __syncthreads();
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK, sKt);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV, nullptr);
+    __syncthreads();
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb) {
+      f32x16 st, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[r] = dp[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < DH / 16; ++s) {
+        st = mfma32(ld_frag(sK + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), qf[s], st);
+        dp = mfma32(ld_frag(sV + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), df[s], dp);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kt * KT + kb * 32 + perm_pos(r, half);
+        const bool ok = qv && key < S && (!CAUSAL || key <= q);
+        const float p = ok ? exp2f(st[r] * sl2 - lse) : 0.f;
+        st[r] = p * (dp[r] - dsum);  // dS
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 sf = pack8(st, j);
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db)
+          dq[db] = mfma32(perm_frag(sKt, db * 32 + l32, kb, j, half), sf, dq[db]);
+      }
+    }
+  }
+  if (qv) {
+    bf16* dst = static_cast<bf16*>(a.dqkv) + (long)(b * S + q) * a.ld_dqkv + hd * DH;
+    store_rows<DH>(dq, scale, a.rope, q, log2theta, half, dst);
+  }
+}
+
+// dK/dV pass (lane = key)
+template <int DH, bool CAUSAL>
+__global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
+  __shared__ __attribute__((aligned(16))) bf16 sQ[KT * (DH + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sQt[DH * TP];
+  __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
+  __shared__ __attribute__((aligned(16))) bf16 sOt[DH * TP];
+  __shared__ float sL[KT], sD[KT];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
+  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int key = blockIdx.x * 128 + wave * 32 + l32;
+  const bool kv = key < S;
+  const int d = a.H * DH;
+  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+  const bf16* dO = static_cast<const bf16*>(a.dout);
+  const long krow = (long)(b * S + (kv ? key : 0));
+
+  bf16x8 kf[DH / 16], vf[DH / 16];
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + d + hd * DH, key, kv, a.rope, log2theta, half, kf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + 2 * d + hd * DH, key, kv, false, 0.f, half, vf);
+
+  f32x16 dk[DH / 32], dv[DH / 32];
+#pragma unroll
+  for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.f;
+
+  const int nqt = (S + KT - 1) / KT;
+  const int qt0 = CAUSAL ? (blockIdx.x * 128) / KT : 0;
+  for (int qt = qt0; qt < nqt; ++qt) {
+    __syncthreads();
+    load_tile<DH>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ, sQt);
+    load_tile<DH>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO, sOt);
+    for (int i = threadIdx.x; i < KT; i += blockDim.x) {
+      const int qq = qt * KT + i;
+      sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
+      sD[i] = qq < S ? a.dsum[(long)bh * S + qq] : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int qb = 0; qb < 2; ++qb) {
+      f32x16 st, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[r] = dp[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < DH / 16; ++s) {
+        st = mfma32(ld_frag(sQ + (qb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), kf[s], st);
+        dp = mfma32(ld_frag(sO + (qb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), vf[s], dp);
+      }
+      f32x16 ds;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int qi = qb * 32 + perm_pos(r, half), qq = qt * KT + qi;
+        const bool ok = kv && qq < S && (!CAUSAL || key <= qq);
+        const float p = ok ? exp2f(st[r] * sl2 - sL[qi]) : 0.f;
+        st[r] = p;
+        ds[r] = p * (dp[r] - sD[qi]);
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 pf = pack8(st, j), sf = pack8(ds, j);
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db) {
+          dv[db] = mfma32(perm_frag(sOt, db * 32 + l32, qb, j, half), pf, dv[db]);
+          dk[db] = mfma32(perm_frag(sQt, db * 32 + l32, qb, j, half), sf, dk[db]);
+        }
+      }
+    }
+  }
+  if (kv) {
+    bf16* dst = static_cast<bf16*>(a.dqkv) + (long)(b * S + key) * a.ld_dqkv;
+    store_rows<DH>(dk, scale, a.rope, key, log2theta, half, dst + d + hd * DH);
+    store_rows<DH>(dv, 1.f, false, key, 0.f, half, dst + 2 * d + hd * DH);
+  }
+}
+
+// ================================================================ fp32 (small stages)
+// One workgroup per (batch, head), one thread per query (forward, dQ) or key
+// (dK, dV); head dim <= 128.
+__device__ __forceinline__ float rot_ld(const float* row, int i, int dh, int pos, bool rot,
+                                        float log2theta) {
+  if (!rot) return row[i];
+  const int h2 = dh / 2, j = i < h2 ? i : i - h2;
+  float cs, sn;
+  rope_cs(pos, j, dh, log2theta, &cs, &sn);
+  const float x1 = row[j], x2 = row[j + h2];
+  return i < h2 ? x1 * cs - x2 * sn : x2 * cs + x1 * sn;
+}
+
+__global__ __launch_bounds__(256) void attn_fwd_f32(AttnArgs a) {
+  const int bh = blockIdx.x, b = bh / a.H, hd = bh % a.H, S = a.S, DH = a.dh, d = a.H * DH;
+  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float sl2 = kLog2e * rsqrtf((float)DH);
+  const float* qkv = static_cast<const float*>(a.qkv);
+  for (int q = threadIdx.x; q < S; q += blockDim.x) {
+    const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
+    float qv[128];
+    for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, log2theta);
+    const int kend = a.causal ? q + 1 : S;
+    float m = -INFINITY;
+    for (int k = 0; k < kend; ++k) {
+      const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
+      float sdot = 0.f;
+      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+      m = fmaxf(m, sdot * sl2);
+    }
+    float l = 0.f, o[128];
+    for (int i = 0; i < DH; ++i) o[i] = 0.f;
+    for (int k = 0; k < kend; ++k) {
+      const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
+      const float* vr = kr + d;
+      float sdot = 0.f;
+      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+      const float p = exp2f(sdot * sl2 - m);
+      l += p;
+      for (int i = 0; i < DH; ++i) o[i] += p * vr[i];
+    }
+    float* orow = static_cast<float*>(a.o) + (long)(b * S + q) * a.ld_o + hd * DH;
+    for (int i = 0; i < DH; ++i) orow[i] = o[i] / l;
+    a.lse[(long)bh * S + q] = m + log2f(l);
+  }
+}
+
+__global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
+  extern __shared__ float sD[];  // [S]
+  const int bh = blockIdx.x, b = bh / a.H, hd = bh % a.H, S = a.S, DH = a.dh, d = a.H * DH;
+  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
+  const float* qkv = static_cast<const float*>(a.qkv);
+  const float* O = static_cast<const float*>(a.o);
+  const float* dO = static_cast<const float*>(a.dout);
+  float* dqkv = static_cast<float*>(a.dqkv);
+  auto score = [&](int q, int k, const float* qv) {
+    const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
+    float sdot = 0.f;
+    for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+    return exp2f(sdot * sl2 - a.lse[(long)bh * S + q]);
+  };
+  auto dpdot = [&](int q, int k) {
+    const float* vr = qkv + (long)(b * S + k) * a.ld_qkv + 2 * d + hd * DH;
+    const float* dr = dO + (long)(b * S + q) * a.ld_do + hd * DH;
+    float s = 0.f;
+    for (int i = 0; i < DH; ++i) s += dr[i] * vr[i];
+    return s;
+  };
+  for (int q = threadIdx.x; q < S; q += blockDim.x) {
+    const float* orow = O + (long)(b * S + q) * a.ld_o + hd * DH;
+    const float* drow = dO + (long)(b * S + q) * a.ld_do + hd * DH;
+    float s = 0.f;
+    for (int i = 0; i < DH; ++i) s += orow[i] * drow[i];
+    sD[q] = s;
+    a.dsum[(long)bh * S + q] = s;
+  }
+  __syncthreads();
+  float buf[128], acc[128];
+  // dQ
+  for (int q = threadIdx.x; q < S; q += blockDim.x) {
+    const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
+    for (int i = 0; i < DH; ++i) { buf[i] = rot_ld(qr, i, DH, q, a.rope, log2theta); acc[i] = 0.f; }
+    const int kend = a.causal ? q + 1 : S;
+    for (int k = 0; k < kend; ++k) {
+      const float ds = score(q, k, buf) * (dpdot(q, k) - sD[q]);
+      const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
+      for (int i = 0; i < DH; ++i) acc[i] += ds * rot_ld(kr, i, DH, k, a.rope, log2theta);
+    }
+    float* dst = dqkv + (long)(b * S + q) * a.ld_dqkv + hd * DH;
+    for (int i = 0; i < DH; ++i) acc[i] *= scale;
+    if (a.rope) {
+      for (int j = 0; j < DH / 2; ++j) {
+        float cs, sn;
+        rope_cs(q, j, DH, log2theta, &cs, &sn);
+        const float d1 = acc[j], d2 = acc[j + DH / 2];
+        acc[j] = d1 * cs + d2 * sn;
+        acc[j + DH / 2] = d2 * cs - d1 * sn;
+      }
+    }
+    for (int i = 0; i < DH; ++i) dst[i] = acc[i];
+  }
+  // dK, dV
+  for (int k = threadIdx.x; k < S; k += blockDim.x) {
+    for (int i = 0; i < DH; ++i) buf[i] = acc[i] = 0.f;  // buf = dV, acc = dK
+    const int qbeg = a.causal ? k : 0;
+    for (int q = qbeg; q < S; ++q) {
+      const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
+      float qv[128];
+      for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, log2theta);
+      const float p = score(q, k, qv);
+      const float ds = p * (dpdot(q, k) - sD[q]);
+      const float* dr = dO + (long)(b * S + q) * a.ld_do + hd * DH;
+      for (int i = 0; i < DH; ++i) { buf[i] += p * dr[i]; acc[i] += ds * qv[i]; }
+    }
+    float* dst = dqkv + (long)(b * S + k) * a.ld_dqkv;
+    for (int i = 0; i < DH; ++i) acc[i] *= scale;
+    if (a.rope) {
+      for (int j = 0; j < DH / 2; ++j) {
+        float cs, sn;
+        rope_cs(k, j, DH, log2theta, &cs, &sn);
+        const float d1 = acc[j], d2 = acc[j + DH / 2];
+        acc[j] = d1 * cs + d2 * sn;
+        acc[j + DH / 2] = d2 * cs - d1 * sn;
+      }
+    }
+    for (int i = 0; i < DH; ++i) { dst[d + hd * DH + i] = acc[i]; dst[2 * d + hd * DH + i] = buf[i]; }
+  }
+}
+
+// ================================================================ launchers
+static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+template <int DH>
+static hipError_t fwd_dh(const AttnArgs& a, hipStream_t s) {
+  dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
+  if (a.causal) hipLaunchKernelGGL((attn_fwd_bf16<DH, true>), grid, block, 0, s, a);
+  else hipLaunchKernelGGL((attn_fwd_bf16<DH, false>), grid, block, 0, s, a);
+  return hipGetLastError();
+}
+template <int DH>
+static hipError_t bwd_dh(const AttnArgs& a, hipStream_t s) {
+  dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
+  if (a.causal) {
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<DH, true>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<DH, true>), grid, block, 0, s, a);
+  } else {
+    hipLaunchKernelGGL((attn_bwd_dq_bf16<DH, false>), grid, block, 0, s, a);
+    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<DH, false>), grid, block, 0, s, a);
+  }
+  return hipGetLastError();
+}
+
+static hipError_t check(int dtype, const AttnArgs& a, bool bwd) {
+  if (a.B <= 0 || a.S <= 0 || a.H <= 0 || !a.qkv || !a.o || !a.lse) return hipErrorInvalidValue;
+  if (bwd && (!a.dout || !a.dsum || !a.dqkv)) return hipErrorInvalidValue;
+  if (dtype == DT_BF16) {
+    if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
+    if (a.ld_qkv % 8 || a.ld_o % 8 || !al16(a.qkv) || !al16(a.o)) return hipErrorInvalidValue;
+    if (bwd && (a.ld_do % 8 || a.ld_dqkv % 4 || !al16(a.dout))) return hipErrorInvalidValue;
+  } else {
+    if (a.dh > 128 || a.dh % 2 || a.S > 4096) return hipErrorInvalidValue;
+  }
+  return hipSuccess;
+}
+
+hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  hipError_t e = check(dtype, a, false);
+  if (e != hipSuccess) return e;
+  if (dtype == DT_BF16) return a.dh == 64 ? fwd_dh<64>(a, s) : fwd_dh<128>(a, s);
+  hipLaunchKernelGGL(attn_fwd_f32, dim3(a.B * a.H), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+  hipError_t e = check(dtype, a, true);
+  if (e != hipSuccess) return e;
+  if (dtype == DT_BF16) return a.dh == 64 ? bwd_dh<64>(a, s) : bwd_dh<128>(a, s);
+  hipLaunchKernelGGL(attn_bwd_f32, dim3(a.B * a.H), dim3(256), a.S * sizeof(float), s, a);
+  return hipGetLastError();
+}
+
+}  // namespace rg

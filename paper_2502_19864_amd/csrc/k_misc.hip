@@ -1,0 +1,285 @@
+// Row-wise RMSNorm, parameter layout kernels, the adapter update and the
+// initiator's loss helpers.
+#include "common.h"
+#include "kernels.h"
+
+namespace rg {
+
+template <typename T>
+__device__ float blk_sum(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+  __syncthreads();
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  float t = 0.f;
+  for (int w = 0; w < nw; ++w) t += red[w];
+  return t;
+}
+
+// ---------------------------------------------------------------- RMSNorm (one workgroup per row)
+template <typename T>
+__global__ __launch_bounds__(256) void rms_fwd_k(int d, float eps, const T* x, const T* g, T* out,
+                                                  T* xhat, float* rstd) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  float ss = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float v = St<T>::ld(x, row + i);
+    ss += v * v;
+  }
+  const float rs = rsqrtf(blk_sum<T>(ss, red) / d + eps);
+  if (rstd && threadIdx.x == 0) rstd[blockIdx.x] = rs;
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float xh = St<T>::ld(x, row + i) * rs;
+    St<T>::st(out, row + i, xh * St<T>::ld(g, i));
+    if (xhat) St<T>::st(xhat, row + i, xh);
+  }
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void rms_bwd_k(int d, const T* dn, const T* dres, const T* xhat,
+                                                  const float* rstd, const T* g, T* dx) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  float s = 0.f;
+  for (int i = threadIdx.x; i < d; i += blockDim.x)
+    s += St<T>::ld(dn, row + i) * St<T>::ld(g, i) * St<T>::ld(xhat, row + i);
+  const float m2 = blk_sum<T>(s, red) / d, rs = rstd[blockIdx.x];
+  for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    const float gg = St<T>::ld(dn, row + i) * St<T>::ld(g, i);
+    St<T>::st(dx, row + i, St<T>::ld(dres, row + i) + rs * (gg - St<T>::ld(xhat, row + i) * m2));
+  }
+}
+
+hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g, void* out,
+                          void* xhat, float* rstd, hipStream_t s) {
+  if (T < 0 || d <= 0 || !x || !g || !out) return hipErrorInvalidValue;
+  if (T == 0) return hipSuccess;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(rms_fwd_k<bf16>, dim3(T), dim3(256), 0, s, d, eps, (const bf16*)x,
+                       (const bf16*)g, (bf16*)out, (bf16*)xhat, rstd);
+  else
+    hipLaunchKernelGGL(rms_fwd_k<float>, dim3(T), dim3(256), 0, s, d, eps, (const float*)x,
+                       (const float*)g, (float*)out, (float*)xhat, rstd);
+  return hipGetLastError();
+}
+
+hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* dres, const void* xhat,
+                          const float* rstd, const void* g, void* dx, hipStream_t s) {
+  if (T < 0 || d <= 0 || !dn || !dres || !xhat || !rstd || !g || !dx) return hipErrorInvalidValue;
+  if (T == 0) return hipSuccess;
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(rms_bwd_k<bf16>, dim3(T), dim3(256), 0, s, d, (const bf16*)dn,
+                       (const bf16*)dres, (const bf16*)xhat, rstd, (const bf16*)g, (bf16*)dx);
+  else
+    hipLaunchKernelGGL(rms_bwd_k<float>, dim3(T), dim3(256), 0, s, d, (const float*)dn,
+                       (const float*)dres, (const float*)xhat, rstd, (const float*)g, (float*)dx);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- layouts
+template <typename Ti, typename To>
+__global__ __launch_bounds__(256) void transpose_k(const Ti* in, int rows, int cols, To* out) {
+  __shared__ float tile[32][33];
+  const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32, tx = threadIdx.x % 32, ty = threadIdx.x / 32;
+  for (int i = ty; i < 32; i += 8) {
+    const int r = r0 + i, c = c0 + tx;
+    tile[i][tx] = (r < rows && c < cols) ? St<Ti>::ld(in, (long)r * cols + c) : 0.f;
+  }
+  __syncthreads();
+  for (int i = ty; i < 32; i += 8) {
+    const int c = c0 + i, r = r0 + tx;
+    if (c < cols && r < rows) St<To>::st(out, (long)c * rows + r, tile[tx][i]);
+  }
+}
+
+hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int rows, int cols, void* out,
+                            hipStream_t s) {
+  if (!in || !out || rows <= 0 || cols <= 0) return hipErrorInvalidValue;
+  const dim3 grid((cols + 31) / 32, (rows + 31) / 32), block(256);
+  if (in_dtype == DT_F32 && out_dtype == DT_F32)
+    hipLaunchKernelGGL((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out);
+  else if (in_dtype == DT_F32 && out_dtype == DT_BF16)
+    hipLaunchKernelGGL((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out);
+  else if (in_dtype == DT_BF16 && out_dtype == DT_BF16)
+    hipLaunchKernelGGL((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out);
+  else
+    return hipErrorInvalidValue;
+  return hipGetLastError();
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void pack_swiglu_k(const T* wgu, int d, int F, T* out) {
+  const long n = 2L * F * d;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < n; idx += (long)gridDim.x * blockDim.x) {
+    const int p = (int)(idx / d), i = (int)(idx % d);
+    const int blk = p / 64, w = p % 64;
+    const int col = w < 32 ? blk * 32 + w : F + blk * 32 + (w - 32);
+    out[idx] = wgu[(long)i * 2 * F + col];
+  }
+}
+
+hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s) {
+  if (!w_gu || !out || d <= 0 || F <= 0 || F % 32) return hipErrorInvalidValue;
+  const dim3 grid(4096), block(256);
+  if (dtype == DT_BF16) hipLaunchKernelGGL(pack_swiglu_k<bf16>, grid, block, 0, s, (const bf16*)w_gu, d, F, (bf16*)out);
+  else hipLaunchKernelGGL(pack_swiglu_k<float>, grid, block, 0, s, (const float*)w_gu, d, F, (float*)out);
+  return hipGetLastError();
+}
+
+// ---------------------------------------------------------------- adapter update
+// Element idx < d*m is W_down[i][j] (i = idx / m, j = idx % m); the rest is
+// W_up[j][i].  Writes the working copies W, W^T in the stage dtype.
+template <typename T, bool UPDATE>
+__global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots, int d, int m, float lr) {
+  const AdapterSlot sl = slots[blockIdx.y];
+  const long n = (long)d * m;
+  for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < 2 * n; idx += (long)gridDim.x * blockDim.x) {
+    if (idx < n) {
+      const int i = (int)(idx / m), j = (int)(idx % m);
+      float w = sl.w_down[idx];
+      if (UPDATE) {
+        w -= lr * sl.g_down[idx];
+        sl.w_down[idx] = w;
+        sl.g_down[idx] = 0.f;
+      }
+      St<T>::st(static_cast<T*>(sl.wdn), idx, w);
+      St<T>::st(static_cast<T*>(sl.wdn_t), (long)j * d + i, w);
+    } else {
+      const long k = idx - n;
+      const int j = (int)(k / d), i = (int)(k % d);
+      float w = sl.w_up[k];
+      if (UPDATE) {
+        w -= lr * sl.g_up[k];
+        sl.w_up[k] = w;
+        sl.g_up[k] = 0.f;
+      }
+      St<T>::st(static_cast<T*>(sl.wup), k, w);
+      St<T>::st(static_cast<T*>(sl.wup_t), (long)i * m + j, w);
+    }
+  }
+}
+
+template <bool UPDATE>
+static hipError_t adapter_update(int dtype, const AdapterSlot* slots, int n_slots, int d, int m, float lr,
+                                 hipStream_t s) {
+  if (!slots || n_slots < 0 || d <= 0 || m <= 0) return hipErrorInvalidValue;
+  if (n_slots == 0) return hipSuccess;
+  const long n = 2L * d * m;
+  const dim3 grid((unsigned)((n + 255) / 256 < 256 ? (n + 255) / 256 : 256), n_slots), block(256);
+  if (dtype == DT_BF16) hipLaunchKernelGGL((adapter_update_k<bf16, UPDATE>), grid, block, 0, s, slots, d, m, lr);
+  else hipLaunchKernelGGL((adapter_update_k<float, UPDATE>), grid, block, 0, s, slots, d, m, lr);
+  return hipGetLastError();
+}
+
+hipError_t launch_adapter_sgd(int dtype, const AdapterSlot* slots, int n_slots, int d, int m, float lr,
+                              hipStream_t s) {
+  return adapter_update<true>(dtype, slots, n_slots, d, m, lr, s);
+}
+hipError_t launch_adapter_sync(int dtype, const AdapterSlot* slots, int n_slots, int d, int m,
+                               hipStream_t s) {
+  return adapter_update<false>(dtype, slots, n_slots, d, m, 0.f, s);
+}
+
+// ---------------------------------------------------------------- losses
+template <typename T>
+__global__ __launch_bounds__(1024) void mse_k(const T* y, const T* t, long n, T* dy, float* loss) {
+  __shared__ float red[16];
+  float s = 0.f;
+  const float sc = 2.f / (float)n;
+  for (long i = threadIdx.x; i < n; i += blockDim.x) {
+    const float diff = St<T>::ld(y, i) - St<T>::ld(t, i);
+    St<T>::st(dy, i, sc * diff);
+    s += diff * diff;
+  }
+  s = blk_sum<T>(s, red);
+  if (loss && threadIdx.x == 0) *loss = s / (float)n;
+}
+
+hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy, float* loss, hipStream_t s) {
+  if (!y || !t || !dy || n <= 0) return hipErrorInvalidValue;
+  if (dtype == DT_BF16) hipLaunchKernelGGL(mse_k<bf16>, dim3(1), dim3(1024), 0, s, (const bf16*)y, (const bf16*)t, n, (bf16*)dy, loss);
+  else hipLaunchKernelGGL(mse_k<float>, dim3(1), dim3(1024), 0, s, (const float*)y, (const float*)t, n, (float*)dy, loss);
+  return hipGetLastError();
+}
+
+// workgroup 0: the head over every sample; the others zero dy outside position 0
+template <typename T>
+__global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
+                                                 const float* bh, int C, const int* labels, T* dy,
+                                                 float* gwh, float* gbh, float* loss) {
+  if (blockIdx.x > 0) {
+    const long per = (long)(S - 1) * d, n = (long)B * per;
+    for (long i = (long)(blockIdx.x - 1) * blockDim.x + threadIdx.x; i < n; i += (long)(gridDim.x - 1) * blockDim.x) {
+      const long b = i / per, r = i % per;
+      St<T>::st(dy, b * S * d + d + r, 0.f);
+    }
+    return;
+  }
+  __shared__ float red[4];
+  __shared__ float sl[16];
+  float total = 0.f;
+  for (int b = 0; b < B; ++b) {
+    const long row = (long)b * S * d;
+    for (int c = 0; c < C; ++c) {
+      float p = 0.f;
+      for (int i = threadIdx.x; i < d; i += blockDim.x) p += St<T>::ld(y, row + i) * wh[(long)i * C + c];
+      p = blk_sum<T>(p, red);
+      if (threadIdx.x == 0) sl[c] = p + bh[c];
+    }
+    __syncthreads();
+    float mx = -INFINITY;
+    for (int c = 0; c < C; ++c) mx = fmaxf(mx, sl[c]);
+    float se = 0.f;
+    for (int c = 0; c < C; ++c) se += __expf(sl[c] - mx);
+    const int lab = labels[b];
+    total += -(sl[lab] - mx - __logf(se));
+    float dl[16];
+    for (int c = 0; c < C; ++c) dl[c] = (__expf(sl[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
+    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+      const float yi = St<T>::ld(y, row + i);
+      float g = 0.f;
+      for (int c = 0; c < C; ++c) {
+        g += dl[c] * wh[(long)i * C + c];
+        gwh[(long)i * C + c] += yi * dl[c];
+      }
+      St<T>::st(dy, row + i, g);
+    }
+    if (threadIdx.x == 0)
+      for (int c = 0; c < C; ++c) gbh[c] += dl[c];
+    __syncthreads();
+  }
+  if (loss && threadIdx.x == 0) *loss = total / (float)B;
+}
+
+hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const float* wh, const float* bh,
+                          int C, const int* labels, void* dy, float* gwh, float* gbh, float* loss,
+                          hipStream_t s) {
+  if (!y || !wh || !bh || !labels || !dy || !gwh || !gbh || B <= 0 || S <= 0 || d <= 0 || C < 1 || C > 16)
+    return hipErrorInvalidValue;
+  const dim3 grid(S > 1 ? 1 + 512 : 1), block(256);
+  if (dtype == DT_BF16)
+    hipLaunchKernelGGL(head_ce_k<bf16>, grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
+                       (bf16*)dy, gwh, gbh, loss);
+  else
+    hipLaunchKernelGGL(head_ce_k<float>, grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels,
+                       (float*)dy, gwh, gbh, loss);
+  return hipGetLastError();
+}
+
+__global__ __launch_bounds__(256) void sgd_f32_k(float* w, float* g, long n, float lr) {
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x) {
+    w[i] -= lr * g[i];
+    g[i] = 0.f;
+  }
+}
+
+hipError_t launch_sgd_f32(float* w, float* g, long n, float lr, hipStream_t s) {
+  if (!w || !g || n <= 0) return hipErrorInvalidValue;
+  const long nb = (n + 255) / 256;
+  hipLaunchKernelGGL(sgd_f32_k, dim3((unsigned)(nb < 1024 ? nb : 1024)), dim3(256), 0, s, w, g, n, lr);
+  return hipGetLastError();
+}
+
+}  // namespace rg

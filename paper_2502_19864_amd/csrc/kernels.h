@@ -1,0 +1,150 @@
+// Host-side launchers of the RingAda kernels (internal to libringada).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace rg {
+
+enum { DT_F32 = 0, DT_BF16 = 1 };
+
+// ---------------------------------------------------------------- GEMM
+// C[M, N] = A[M, K] * B[N, K]^T followed by an epilogue.  Both operands are
+// K-contiguous (row strides lda, ldb in elements).
+enum class Epi {
+  Store,    // out = acc (+ bias[n])
+  Gelu,     // pre = acc (+ bias[n]); out2 = pre (if non-null); out = gelu(pre)
+  Resid,    // out = acc + aux[m, n]
+  DGelu,    // out = acc * gelu'(aux[m, n])
+  SwiGlu,   // B rows packed [gate 32 | up 32] per 64; out[m, f] = silu(gate) * up,
+            // out2[m, f] = gate, out2[m, half + f] = up (if non-null)
+  DSwiGlu,  // acc = d(act)[m, f]; aux = [gate | up]; out[m, f] = d gate,
+            // out[m, half + f] = d up
+};
+
+struct GemmArgs {
+  const void* A; int lda;
+  const void* B; int ldb;
+  int M, N, K;
+  const void* bias;
+  const void* aux; int ld_aux;
+  void* out; int ldo;
+  void* out2; int ldo2;
+  int half;
+};
+
+// Names of the GEMM call sites (each gets its own kernel symbol).
+enum Role {
+  R_QKV_FWD, R_O_FWD, R_FFN_IN_FWD, R_FFN_OUT_FWD,
+  R_QKV_DX, R_O_DX, R_FFN_IN_DX, R_FFN_OUT_DX, N_ROLES
+};
+const char* role_name(Role r);
+
+// Returns hipErrorInvalidValue if the shapes or alignments do not fit the
+// kernel (checked on the host before any launch).
+hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- attention
+struct AttnArgs {
+  int B, S, H, dh;
+  int causal, rope;
+  float theta;
+  const void* qkv; int ld_qkv;  // [B*S, ld] with Q at column 0, K at d, V at 2d
+  void* o; int ld_o;            // [B*S, d]
+  float* lse;                   // [B, H, S]
+  // backward
+  const void* dout; int ld_do;  // dO [B*S, d]
+  float* dsum;                  // D = rowsum(dO * O) [B, H, S] (written by dq pass)
+  void* dqkv; int ld_dqkv;      // [B*S, 3d]
+};
+hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s);
+hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- adapters (Eq. (1)) fused with the residual add and the norm
+enum class Norm { LN, RMS, None };
+struct AdapterFwdArgs {
+  int T, d, m;
+  Norm norm;
+  float eps;
+  const void* z;      // adapter input [T, d]
+  const void* res;    // residual [T, d]
+  const void* wdn_t;  // W_down^T [m, d] (stage dtype)
+  const void* wup_t;  // W_up^T   [d, m]
+  const void* gamma;  // [d]
+  const void* beta;   // [d] (LN)
+  void* out;          // LN: LN(res + adapter(z)); RMS: h = res + adapter(z); None: same
+  void* out_norm;     // RMS: h_norm = RMSNorm(h) * gamma
+  void* u;            // stash of z W_down [T, m] (may be null)
+  void* xhat;         // stash of the normalised input [T, d] (may be null)
+  float* rstd;        // stash [T] (may be null)
+};
+hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s);
+
+struct AdapterBwdArgs {
+  int T, d, m;
+  Norm norm;          // LN: gin is the LN-output gradient; RMS: gin is the
+                      // gradient at the RMSNorm output and dres is added;
+                      // None: gin is the adapter-output gradient
+  const void* gin;    // [T, d]
+  const void* dres;   // [T, d] (RMS only)
+  const void* xhat;   // [T, d]
+  const float* rstd;  // [T]
+  const void* gamma;  // [d]
+  const void* u;      // stash z W_down [T, m]
+  const void* wup;    // W_up [m, d]
+  const void* wdn;    // W_down [d, m]
+  void* dz;           // gradient at the adapter output [T, d]; may be null for
+                      // Norm::None (it equals gin)
+  void* du;           // gradient at z W_down [T, m] (always written)
+  void* dzin;         // gradient at the adapter input [T, d]; null = skip
+};
+hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s);
+
+// dW_up[m, d] += gelu(U)^T dZ ; dW_down[d, m] += Z^T dU   (fp32 accumulators)
+struct AdapterDwArgs {
+  int T, d, m;
+  const void* u;   // [T, m]
+  const void* dz;  // [T, d]
+  const void* z;   // [T, d]
+  const void* du;  // [T, m]
+  float* g_up;     // [m, d]
+  float* g_down;   // [d, m]
+};
+hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s);
+
+// ---------------------------------------------------------------- row kernels
+// out = RMSNorm(x) * g, xhat/rstd stashes optional
+hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g,
+                          void* out, void* xhat, float* rstd, hipStream_t s);
+// dx = dres + RMSNorm'(dn)
+hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* dres,
+                          const void* xhat, const float* rstd, const void* g, void* dx,
+                          hipStream_t s);
+
+// ---------------------------------------------------------------- parameters
+// out[c, r] = in[r, c] (rows x cols), converting float -> stage dtype
+hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int rows, int cols,
+                            void* out, hipStream_t s);
+// pack W_gu [d, 2F] into B rows for the SwiGlu epilogue: row p of the result
+// (2F x d) is gate column (p/64)*32 + p%32 if p%64 < 32, else the matching up column
+hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s);
+
+struct AdapterSlot {  // device-side table entry for the update kernel
+  float* w_down; float* w_up; float* g_down; float* g_up;
+  void* wdn; void* wdn_t; void* wup; void* wup_t;  // working copies
+};
+// SGD on n_slots adapters, zero grads, refresh working copies
+hipError_t launch_adapter_sgd(int dtype, const AdapterSlot* slots_dev, int n_slots, int d, int m,
+                              float lr, hipStream_t s);
+// refresh working copies only
+hipError_t launch_adapter_sync(int dtype, const AdapterSlot* slots_dev, int n_slots, int d, int m,
+                               hipStream_t s);
+
+// ---------------------------------------------------------------- losses
+hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy, float* loss,
+                      hipStream_t s);
+hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const float* wh,
+                          const float* bh, int C, const int* labels, void* dy, float* gwh,
+                          float* gbh, float* loss, hipStream_t s);
+hipError_t launch_sgd_f32(float* w, float* g, long n, float lr, hipStream_t s);
+
+}  // namespace rg

@@ -1,0 +1,63 @@
+"""Test helpers: running the oracle on a workload's inputs, and the parity
+measure.  Only tests/, the smoke check and the benchmark's CPU leg use this."""
+from __future__ import annotations
+
+import numpy as np
+
+import oracle as O
+from paper_2502_19864_amd.workloads import adapters_as_computed
+
+TOL = {"f32": 1e-4, "bf16": 2e-2}
+
+
+def rel_err(got, ref):
+    """max |got - ref| / max |ref| over one output tensor."""
+    got = np.asarray(got, dtype=np.float64)
+    ref = np.asarray(ref, dtype=np.float64)
+    assert got.shape == ref.shape, (got.shape, ref.shape)
+    den = np.abs(ref).max()
+    return float(np.abs(got - ref).max() / (den if den > 0 else 1.0))
+
+
+def oracle_desc(w):
+    return O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter)
+
+
+def to64(inp, w):
+    W = [{k: v.astype(np.float64) for k, v in b.items()} for b in inp["weights"]]
+    A = [tuple({k: v.astype(np.float64) for k, v in a.items()} for a in pair)
+         for pair in adapters_as_computed(w, inp["adapters"])]
+    return W, A
+
+
+def oracle_run(w, inp, c, dy=None, x=None, batch=None, seq=None):
+    """Forward + loss + early-stopped backward in float64.  `batch`/`seq`
+    restrict the run to x[:batch, :seq] (valid for batch-independence and,
+    with causal attention, for a sequence prefix)."""
+    desc = oracle_desc(w)
+    W, A = to64(inp, w)
+    x = inp["x"] if x is None else x
+    x = np.asarray(x, np.float64)
+    if batch is not None:
+        x = x[:batch]
+    if seq is not None:
+        x = x[:, :seq]
+    y, caches = O.stage_forward(desc, W, A, x)
+    out = {"y": y}
+    if dy is None:
+        if w.loss == "mse":
+            out["loss"], dy = O.mse_loss(y, inp["target"].astype(np.float64))
+        elif w.loss == "cls_ce":
+            lab = inp["labels"] if batch is None else inp["labels"][:batch]
+            out["loss"], dy, out["g_wh"], out["g_bh"] = O.cls_head_ce(
+                y, inp["w_h"].astype(np.float64), inp["b_h"].astype(np.float64), lab)
+        else:
+            dy = inp["dy"].astype(np.float64)
+    dy = np.asarray(dy, np.float64)
+    if batch is not None and dy.shape[0] != x.shape[0]:
+        dy = dy[:batch]
+    if seq is not None and dy.shape[1] != x.shape[1]:
+        dy = dy[:, :seq]
+    out["dy"] = dy
+    out["dx"], out["grads"] = O.stage_backward(desc, W, A, caches, dy, c)
+    return out

@@ -1,0 +1,122 @@
+"""Host-only checks of the C ABI (no GPU needed): the library loads and exports
+every declared symbol; the planner, the cut-off mapping and argument
+validation behave as documented in include/ringada.h."""
+import os
+import re
+
+import pytest
+
+from paper_2502_19864_amd import binding as B
+from paper_2502_19864_amd.stage import make_desc
+from paper_2502_19864_amd.workloads import SWEEP, WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+MiB = 1 << 20
+
+
+def header_symbols():
+    txt = open(os.path.join(ROOT, "include", "ringada.h")).read()
+    txt = re.sub(r"/\*.*?\*/", "", txt, flags=re.S)
+    return sorted(set(re.findall(r"\b(ringada_[a-z0-9_]+)\s*\(", txt)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = B.lib()
+    syms = header_symbols()
+    assert len(syms) >= 15
+    for s in syms:
+        assert hasattr(L, s), s
+    # the binding declares exactly the header's functions
+    assert sorted(n for n, _, _ in B.SIGNATURES) == syms
+
+
+def plan_mib(wname, c, batch=None, seq=None):
+    w = WORKLOADS[wname]
+    st, sc = B.ringada_stage_plan(make_desc(w), batch or w.batch, seq or w.seq, c)
+    return st / MiB, sc / MiB
+
+
+def test_stash_planner_bert_base_sweep():
+    # stash bytes per cut-off for the BERT-base stage (T = 4096, d = 768, F = 3072,
+    # m = 64): a full block keeps qkv, o, lse, attn, u1, xhat1, rstd1, a1, f2,
+    # u2, xhat2, rstd2 = 73.2 MiB; the cut-off block drops qkv, o, lse = 49.0 MiB
+    expect = {11: 49.0, 9: 195.5, 8: 268.7, 6: 415.1, 3: 634.8, 0: 854.4, -1: 878.6}
+    for c, mib in expect.items():
+        got, _ = plan_mib("bert_base", c)
+        assert abs(got - mib) < 0.05, (c, got, mib)
+    assert set(SWEEP) <= set(expect)
+
+
+def test_stash_planner_other_workloads():
+    assert abs(plan_mib("llama7b_share", 6)[0] - 349.3) < 0.1
+    assert abs(plan_mib("bert_large_share", 3)[0] - 259.6) < 0.1
+    # a frozen stage stashes nothing; the tiny stage at c = 0 stashes 1.3 MiB
+    assert plan_mib("bert_base", 12)[0] == 0
+    assert plan_mib("bert_base", 100)[0] == 0
+    assert abs(plan_mib("tiny", 0)[0] - 1.3) < 0.05
+
+
+def test_stash_is_monotone_in_the_cutoff():
+    prev = None
+    for c in range(12, -2, -1):
+        st, sc = plan_mib("bert_base", c)
+        assert prev is None or st >= prev
+        prev = st
+        assert sc > 0
+
+
+def test_local_cutoff_matches_the_four_client_example():
+    # 4:5:2:3 blocks over 14, depth 3: clients 1..3 forward-only, client 4
+    # terminator at its first block
+    starts, sizes = [0, 4, 9, 11], [4, 5, 2, 3]
+    got = [B.ringada_local_cutoff(14, 3, s, n) for s, n in zip(starts, sizes)]
+    assert got == [4, 5, 2, 0]
+    # deeper unfreezing: the cut-off moves into client 2 (block 6 of 14 for depth 9)
+    got = [B.ringada_local_cutoff(14, 9, s, n) for s, n in zip(starts, sizes)]
+    assert got == [4, 1, -1, -1]
+    assert B.ringada_local_cutoff(12, 4, 0, 12) == 8
+    assert B.ringada_local_cutoff(12, 0, 0, 12) == 12
+    assert B.ringada_local_cutoff(0, 1, 0, 1) < -1000
+    assert B.ringada_local_cutoff(10, 11, 0, 10) < -1000
+
+
+def test_plan_and_create_validate_arguments():
+    w = WORKLOADS["bert_base"]
+    desc = make_desc(w)
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_plan(desc, w.batch + 1, w.seq, 8)
+    assert e.value.status == B.RINGADA_E_INVALID
+    bad = make_desc(w)
+    bad.d_adapter = 48
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_create(bad)
+    assert e.value.status == B.RINGADA_E_UNSUPPORTED
+    bad = make_desc(w)
+    bad.n_heads = 7
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_plan(bad, 1, 1, 0)
+    assert e.value.status == B.RINGADA_E_INVALID
+    bad = make_desc(WORKLOADS["llama7b_share"])
+    bad.dtype = B.F32
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_create(bad)
+    assert e.value.status == B.RINGADA_E_UNSUPPORTED
+
+
+def test_state_machine_on_an_unbound_stage():
+    """Calls out of order fail with E_STATE before touching the device."""
+    w = WORKLOADS["tiny"]
+    h = B.ringada_stage_create(make_desc(w))
+    try:
+        with pytest.raises(B.RingadaError) as e:
+            B.ringada_stage_forward(h, None, 16, 4096, w.batch, w.seq, 0, 0, 0, 0, 0)
+        assert e.value.status == B.RINGADA_E_STATE          # blocks not bound
+        with pytest.raises(B.RingadaError) as e:
+            B.ringada_stage_backward(h, None, 16, 0, None)
+        assert e.value.status == B.RINGADA_E_STATE          # nothing pending
+        with pytest.raises(B.RingadaError) as e:
+            B.ringada_adapter_step(h, None, 0, 0.1, kind=1)
+        assert e.value.status == B.RINGADA_E_UNSUPPORTED    # only SGD
+        assert "SGD" in B.ringada_last_error()
+    finally:
+        B.ringada_stage_destroy(h)
