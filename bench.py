@@ -1,0 +1,183 @@
+"""Benchmark of the RingAda stage hot path on one MI355X.
+
+One step = the whole per-stage path on one batch of synthetic input resident
+in HBM: forward through the 12-block BERT-base-shaped stage, the initiator's
+[CLS]-head loss and head update, the backward stopped at block 8, and the
+update of the unfrozen adapters.  Prints one JSON line.
+
+    python bench.py [--steps K] [--warmup W] [--gpus 1] [--workload NAME]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "stage fine-tune samples/sec (fwd+early-stop bwd); % bf16 MFMA peak"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
+GEMM_PREFIX = "gemm_"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def cpu_baseline(w, inp):
+    """The float oracle timed on this host: one full step (forward, head loss,
+    early-stopped backward, SGD) on every sample of the workload, fp32."""
+    import oracle as O
+    from threadpoolctl import threadpool_info
+    from paper_2502_19864_amd.workloads import adapters_as_computed
+    desc = O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter)
+    W = inp["weights"]
+    A = adapters_as_computed(w, inp["adapters"])
+    t0 = time.perf_counter()
+    y, caches = O.stage_forward(desc, W, A, inp["x"])
+    if w.loss == "cls_ce":
+        _, dy, _, _ = O.cls_head_ce(y, inp["w_h"], inp["b_h"], inp["labels"])
+    elif w.loss == "mse":
+        _, dy = O.mse_loss(y, inp["target"])
+    else:
+        dy = inp["dy"]
+    _, grads = O.stage_backward(desc, W, A, caches, dy, w.lowest_unfrozen)
+    O.sgd_step(A, grads, 1e-3)
+    dt = time.perf_counter() - t0
+    threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
+    return {"value": round(w.batch / dt, 3), "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"one full step (forward, head loss, backward to block {w.lowest_unfrozen}, SGD) of "
+                      f"the {w.name} workload, all {w.batch} samples, numpy float32 oracle, {dt:.2f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="bert_base")
+    ap.add_argument("--lowest-unfrozen", type=int, default=None)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print(f"bench.py: this build runs one ring stage on one GPU; --gpus {args.gpus} is not supported "
+              f"(the multi-GPU ring is not part of it)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2502_19864_amd import binding as B
+    from paper_2502_19864_amd.stage import Stage
+    from paper_2502_19864_amd.workloads import WORKLOADS, make_inputs
+
+    if not torch.cuda.is_available():
+        print("bench.py: no GPU visible", file=sys.stderr)
+        sys.exit(1)
+    B.lib()
+    w = WORKLOADS[args.workload]
+    if args.lowest_unfrozen is not None:
+        w = w.replace(lowest_unfrozen=args.lowest_unfrozen)
+    c = w.lowest_unfrozen
+    log(f"[bench] workload {w.name}: generating inputs")
+    inp = make_inputs(w)
+    st = Stage(w, inp)
+    dev = st.dev
+    x = st.upload(inp["x"])
+    y = st.empty(*inp["x"].shape)
+    dy = st.empty(*inp["x"].shape)
+    dx = st.empty(*inp["x"].shape) if c < 0 else None
+    loss = torch.zeros(1, dtype=torch.float32, device=dev)
+    if w.loss == "cls_ce":
+        wh, bh = st.f32(inp["w_h"]), st.f32(inp["b_h"])
+        gwh, gbh = torch.zeros_like(wh), torch.zeros_like(bh)
+        labels = torch.from_numpy(inp["labels"]).to(dev)
+    elif w.loss == "mse":
+        target = st.upload(inp["target"])
+    else:
+        dy = st.upload(inp["dy"])
+    stash_bytes, scratch_bytes = st.ensure_workspace(w.batch, w.seq, c)
+    s = st.sptr
+    lr = 1e-4
+
+    def step():
+        st.forward(x, y, c)
+        if w.loss == "cls_ce":
+            B.ringada_head_ce(s, st.desc.dtype, y, w.batch, w.seq, w.d_model, wh, bh, 2, labels, dy, gwh, gbh, loss)
+            B.ringada_sgd_f32(s, wh, gwh, wh.numel(), lr)
+            B.ringada_sgd_f32(s, bh, gbh, bh.numel(), lr)
+        elif w.loss == "mse":
+            B.ringada_loss_mse(s, st.desc.dtype, y, target, y.numel(), dy, loss)
+        if c < w.n_blocks:
+            st.backward(dy, c, dx)
+            st.step(c, lr)
+
+    log(f"[bench] warmup {args.warmup} steps")
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps")
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    ms = 1e3 * elapsed / args.steps
+    value = w.batch * args.steps / elapsed
+
+    # per-kernel durations: HIP events around every launch, same steps again
+    log("[bench] per-kernel event timing")
+    B.ringada_prof_begin(st.handle)
+    for _ in range(args.steps):
+        step()
+    prof = B.ringada_prof_end(st.handle, 128)
+    torch.cuda.synchronize()
+    prof.sort(key=lambda e: -e["total_ms"])
+    for e in prof:
+        log("[bench]   %-18s %5d launches %9.3f ms total %8.2f us avg  %7.1f TFLOP/s  %7.1f GB/s" % (
+            e["name"], e["launches"], e["total_ms"], 1e3 * e["total_ms"] / e["launches"],
+            e["flops"] / (e["total_ms"] * 1e-3) / 1e12 if e["total_ms"] else 0,
+            e["bytes"] / (e["total_ms"] * 1e-3) / 1e9 if e["total_ms"] else 0))
+    gemms = [e for e in prof if e["name"].startswith(GEMM_PREFIX)]
+    gemm_flops = sum(e["flops"] for e in gemms)
+    gemm_ms = sum(e["total_ms"] for e in gemms)
+    all_flops = sum(e["flops"] for e in prof)
+    dom = prof[0]
+    dom_avg_s = dom["total_ms"] * 1e-3 / dom["launches"]
+    if dom["flops"] > 0:
+        achieved = dom["flops"] / dom["launches"] / dom_avg_s / 1e12
+        roof = {"kernel": dom["name"], "bound": "mfma", "achieved": round(achieved, 2),
+                "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s", "frac": round(achieved / PEAK_BF16_TFLOPS, 4),
+                "traffic": None, "avg_us": round(dom_avg_s * 1e6, 2), "launches_per_step": dom["launches"] // args.steps}
+    else:
+        achieved = dom["bytes"] / dom["launches"] / dom_avg_s / 1e9
+        roof = {"kernel": dom["name"], "bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
+                "avg_us": round(dom_avg_s * 1e6, 2), "launches_per_step": dom["launches"] // args.steps}
+
+    cpu = None if args.no_cpu_baseline else cpu_baseline(w, inp)
+    st.close()
+    out = {
+        "metric": METRIC, "value": round(value, 2), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
+        "config": {"workload": f"{w.name}: {w.n_blocks} {'post-LN' if w.arch == 'bert' else 'pre-RMSNorm'} "
+                               f"blocks, d={w.d_model}, {w.n_heads} heads, FFN {w.d_ffn}, two adapters/block "
+                               f"m={w.d_adapter}, seq {w.seq}, batch {w.batch}, lowest unfrozen block {c}",
+                   "batch": w.batch, "seq_len": w.seq, "n_blocks": w.n_blocks, "lowest_unfrozen": c,
+                   "parallelism": "one ring stage on one GPU"},
+        "tokens_per_s": round(value * w.seq, 1),
+        "gemm_mfma_frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
+        "stage_mfma_frac": round(all_flops / args.steps / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
+        "stash_bytes": stash_bytes, "scratch_bytes": scratch_bytes,
+        "roofline": roof, "cpu_baseline": cpu,
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

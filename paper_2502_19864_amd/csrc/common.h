@@ -12,12 +12,13 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 __device__ __forceinline__ float bf2f(bf16 b) { return __uint_as_float((uint32_t)b << 16); }
 
-// round to nearest even; NaN stays NaN
-__device__ __forceinline__ bf16 f2bf(float f) {
-  uint32_t u = __float_as_uint(f);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16)((u >> 16) | 0x40);
-  u += 0x7fffu + ((u >> 16) & 1u);
-  return (bf16)(u >> 16);
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+
+// round to nearest even (v_cvt_pk_bf16_f32); NaN stays NaN
+__device__ __forceinline__ bf16 f2bf(float f) { return __builtin_bit_cast(bf16, (__bf16)f); }
+__device__ __forceinline__ uint32_t f2bf2(float lo, float hi) {
+  bf16x2_t v = {(__bf16)lo, (__bf16)hi};
+  return __builtin_bit_cast(uint32_t, v);
 }
 
 // storage abstraction: float or bf16 storage, fp32 arithmetic
@@ -45,8 +46,8 @@ template <> struct St<bf16> {
   }
   static __device__ __forceinline__ void st4(bf16* p, long i, const float v[4]) {
     uint2 q;
-    q.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-    q.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
+    q.x = f2bf2(v[0], v[1]);
+    q.y = f2bf2(v[2], v[3]);
     *reinterpret_cast<uint2*>(p + i) = q;
   }
 };
@@ -82,10 +83,10 @@ __device__ __forceinline__ bf16x8 zero_frag() {
 }
 __device__ __forceinline__ bf16x8 pack_frag(const float v[8]) {
   uint4 q;
-  q.x = (uint32_t)f2bf(v[0]) | ((uint32_t)f2bf(v[1]) << 16);
-  q.y = (uint32_t)f2bf(v[2]) | ((uint32_t)f2bf(v[3]) << 16);
-  q.z = (uint32_t)f2bf(v[4]) | ((uint32_t)f2bf(v[5]) << 16);
-  q.w = (uint32_t)f2bf(v[6]) | ((uint32_t)f2bf(v[7]) << 16);
+  q.x = f2bf2(v[0], v[1]);
+  q.y = f2bf2(v[2], v[3]);
+  q.z = f2bf2(v[4], v[5]);
+  q.w = f2bf2(v[6], v[7]);
   return __builtin_bit_cast(bf16x8, q);
 }
 __device__ __forceinline__ void unpack_frag(bf16x8 f, float v[8]) {
