@@ -64,6 +64,8 @@ def main():
     ap.add_argument("--workload", default="bert_base")
     ap.add_argument("--lowest-unfrozen", type=int, default=None)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="launch every kernel from the host each step instead of replaying a HIP graph")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one ring stage on one GPU; --gpus {args.gpus} is not supported "
@@ -101,10 +103,10 @@ def main():
     else:
         dy = st.upload(inp["dy"])
     stash_bytes, scratch_bytes = st.ensure_workspace(w.batch, w.seq, c)
-    s = st.sptr
     lr = 1e-4
 
     def step():
+        s = st.sptr
         st.forward(x, y, c)
         if w.loss == "cls_ce":
             B.ringada_head_ce(s, st.desc.dtype, y, w.batch, w.seq, w.d_model, wh, bh, 2, labels, dy, gwh, gbh, loss)
@@ -120,10 +122,28 @@ def main():
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
-    log(f"[bench] timing {args.steps} steps")
+    run = step
+    if not args.no_graph:
+        # one step captured into a HIP graph (every launch of the step is
+        # stream-ordered on the capturing stream), replayed each step
+        graph = torch.cuda.CUDAGraph()
+        cap = torch.cuda.Stream()
+        cap.wait_stream(torch.cuda.current_stream())
+        with torch.cuda.stream(cap):
+            step()  # one eager step on the capture stream first
+        torch.cuda.current_stream().wait_stream(cap)
+        torch.cuda.synchronize()
+        with torch.cuda.graph(graph, stream=cap):
+            step()
+        torch.cuda.synchronize()
+        run = graph.replay
+        for _ in range(2):
+            run()
+        torch.cuda.synchronize()
+    log(f"[bench] timing {args.steps} steps ({'HIP graph replay' if run is not step else 'eager launches'})")
     t0 = time.perf_counter()
     for _ in range(args.steps):
-        step()
+        run()
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t0
     ms = 1e3 * elapsed / args.steps
@@ -174,6 +194,7 @@ def main():
         "gemm_mfma_frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
         "stage_mfma_frac": round(all_flops / args.steps / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "stash_bytes": stash_bytes, "scratch_bytes": scratch_bytes,
+        "launch": "hip_graph" if run is not step else "eager",
         "roofline": roof, "cpu_baseline": cpu,
     }
     print(json.dumps(out), flush=True)

@@ -68,7 +68,8 @@ typedef struct {
   int32_t arch;       /* RINGADA_ARCH_* */
   int32_t dtype;      /* RINGADA_F32 or RINGADA_BF16 storage */
   int32_t n_blocks;   /* L, blocks held by this stage, >= 1 */
-  int32_t d_model;    /* d; bf16 path: multiple of 64 and <= 4096 */
+  int32_t d_model;    /* d; bf16 path: a multiple of 256 up to 1024, or of
+                         1024 up to 4096 */
   int32_t n_heads;    /* d_head = d_model / n_heads; bf16 path: d_head 64 or 128 */
   int32_t d_ffn;      /* F; bf16 path: multiple of 64 */
   int32_t d_adapter;  /* m, the bottleneck of Eq. (1); bf16 path: 64 */

@@ -97,6 +97,27 @@ __device__ __forceinline__ void unpack_frag(bf16x8 f, float v[8]) {
   v[6] = __uint_as_float(q.w << 16); v[7] = __uint_as_float(q.w & 0xffff0000u);
 }
 
+// ---------------------------------------------------------------- LDS transpose reads
+typedef short v4i16_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4i16_t* lds_v4i16_ptr;
+// ds_read_b64_tr_b16 over a row-major LDS tile X[k][n] (pitch in elements):
+// for the 16-lane group of this lane, returns X[k0 + 0..3][n0 + lane % 16]
+// as 4 consecutive bf16.  (Within a group, lane r = 4j + q supplies the address
+// of X[k0 + j][n0 + 4q]; the instruction hands lane i element i % 4 of the
+// rows supplied by lanes i/4, 4 + i/4, 8 + i/4, 12 + i/4.)
+__device__ __forceinline__ uint2 lds_tr4(const bf16* tile, int pitch, int k0, int n0, int lane) {
+  const int r = lane & 15;
+  const bf16* p = tile + (k0 + (r >> 2)) * pitch + n0 + 4 * (r & 3);
+  return __builtin_bit_cast(uint2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4i16_ptr)p));
+}
+// MFMA 32x32x16 operand with k contiguous per lane from a row-major [k][n]
+// tile: lane l gets X[k0 + 8*(l/32) + 0..7][n0 + l%32]
+__device__ __forceinline__ bf16x8 lds_tr_frag32(const bf16* tile, int pitch, int k0, int n0, int lane) {
+  const int g = lane >> 4, nn = n0 + 16 * (g & 1), kk = k0 + 8 * (g >> 1);
+  const uint2 lo = lds_tr4(tile, pitch, kk, nn, lane), hi = lds_tr4(tile, pitch, kk + 4, nn, lane);
+  return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
+}
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

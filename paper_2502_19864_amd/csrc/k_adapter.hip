@@ -19,37 +19,90 @@ constexpr int MB = 64;    // adapter bottleneck of the bf16 path
 constexpr int GP = MB + 8;
 
 // ================================================================ bf16 forward
-template <int NW>
+// Workgroup: 16 tokens, NW waves, d = 16 * NW * FB features (wave w owns
+// features [w*16*FB, (w+1)*16*FB)).  Every global load is issued before the
+// first use: the z tile goes to LDS with coalesced 16-B loads, the residual is
+// prefetched into registers, weight fragments come from L2 in unrolled runs.
+template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
-  constexpr int KS = NW / 4;  // k-splits of the down projection
-  __shared__ __attribute__((aligned(16))) bf16 sG[TOK * GP];
-  __shared__ float sUp[KS > 1 ? KS : 1][TOK][MB];
-  __shared__ float sRed[NW][TOK];
+  constexpr int KS = NW / 4;           // k-splits of the down projection
+  constexpr int D = 16 * NW * FB, DP = D + 8;
+  constexpr int SLICE = D / KS;        // k range of one down-projection wave
+  static_assert(SLICE % 32 == 0, "k slice");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  bf16* sZ = reinterpret_cast<bf16*>(smem);                // [TOK][DP]
+  bf16* sG = sZ + TOK * DP;                                // [TOK][GP]
+  float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][TOK][MB]
+  float* sRed = sUp + KS * TOK * MB;                       // [NW][TOK]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
-  const int d = a.d, T = a.T;
-  const int token = blockIdx.x * TOK + l16;
+  const int T = a.T, t0 = blockIdx.x * TOK;
+  const int token = t0 + l16;
   const bool tv = token < T;
-  const long trow = (long)(tv ? token : 0) * d;
+  const long trow = (long)(tv ? token : 0) * D;
   const bf16* z = static_cast<const bf16*>(a.z);
+  const int f0 = wave * 16 * FB;
+
+  // z tile -> LDS
+  {
+    constexpr int CPR = D / 8, NCH = TOK * CPR, PER = (NCH + NW * 64 - 1) / (NW * 64);
+    uint4 v[PER];
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NW * 64, r = c / CPR, k = (c % CPR) * 8;
+      v[i] = (c < NCH && t0 + r < T) ? *reinterpret_cast<const uint4*>(z + (long)(t0 + r) * D + k)
+                                     : make_uint4(0, 0, 0, 0);
+    }
+#pragma unroll
+    for (int i = 0; i < PER; ++i) {
+      const int c = threadIdx.x + i * NW * 64, r = c / CPR, k = (c % CPR) * 8;
+      if (c < NCH) *reinterpret_cast<uint4*>(sZ + r * DP + k) = v[i];
+    }
+  }
+  // residual (phase-2 layout: 4 consecutive features of one token, kept
+  // packed) and the up-projection fragments, all in flight with the z tile
+  uint2 rr[FB];
+#pragma unroll
+  for (int b = 0; b < FB; ++b)
+    rr[b] = tv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + trow + f0 + b * 16 + 4 * grp)
+               : make_uint2(0, 0);
+  // issued early while the registers allow (16-wave workgroups have 128 VGPRs)
+  constexpr bool PRE = FB <= 4;
+  bf16x8 w0[FB], w1[FB];
+  const bf16* wu = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
+  if constexpr (PRE) {
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      w0[b] = ld_frag(wu + (long)b * 16 * MB);
+      w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+    }
+  }
+  __syncthreads();
 
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:]
   {
-    const int ug = wave % 4, ks = wave / 4, slice = d / KS;
-    const bf16* wd = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * d + 8 * grp;
-    const bf16* zr = z + trow + 8 * grp;
+    const int ug = wave % 4, ks = wave / 4;
+    const bf16* wd = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
+    const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
     f32x4 u = {0.f, 0.f, 0.f, 0.f};
-    for (int kk = ks * slice; kk < (ks + 1) * slice; kk += 32)
-      u = mfma16(ld_frag(wd + kk), tv ? ld_frag(zr + kk) : zero_frag(), u);
+    constexpr int NSTEP = SLICE / 32, RUN = NSTEP < 8 ? NSTEP : 8;
+#pragma unroll
+    for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
+      bf16x8 w[RUN];
+#pragma unroll
+      for (int j = 0; j < RUN; ++j) w[j] = ld_frag(wd + (k0 + j) * 32);
+#pragma unroll
+      for (int j = 0; j < RUN; ++j) u = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), u);
+    }
     if constexpr (KS > 1) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sUp[ks][l16][ug * 16 + 4 * grp + r] = u[r];
+      for (int r = 0; r < 4; ++r) sUp[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = u[r];
       __syncthreads();
       if (ks == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
           float s = 0.f;
 #pragma unroll
-          for (int k2 = 0; k2 < KS; ++k2) s += sUp[k2][l16][ug * 16 + 4 * grp + r];
+          for (int k2 = 0; k2 < KS; ++k2) s += sUp[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
           u[r] = s;
         }
       }
@@ -57,47 +110,47 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
     if (ks == 0) {
       float uv[4] = {u[0], u[1], u[2], u[3]};
       if (a.u && tv) St<bf16>::st4(static_cast<bf16*>(a.u), (long)token * MB + ug * 16 + 4 * grp, uv);
+      float gv[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sG[l16 * GP + ug * 16 + 4 * grp + r] = f2bf(gelu_f(uv[r]));
+      for (int r = 0; r < 4; ++r) gv[r] = gelu_f(uv[r]);
+      St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
     }
   }
   __syncthreads();
 
   // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  + z + res
-  const int FW = d / NW, FB = FW / 16, f0 = wave * FW;
-  float v[16][4];
+  float v[FB][4];
   {
-    const bf16* wu = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
     const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+    if constexpr (!PRE) {
 #pragma unroll
-    for (int b = 0; b < 16; ++b) {
-      if (b < FB) {
-        f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-        acc = mfma16(ld_frag(wu + (long)b * 16 * MB), g0, acc);
-        acc = mfma16(ld_frag(wu + (long)b * 16 * MB + 32), g1, acc);
-        const int f = f0 + b * 16 + 4 * grp;
-        float zz[4], rr[4];
-        if (tv) {
-          St<bf16>::ld4(z, trow + f, zz);
-          St<bf16>::ld4(static_cast<const bf16*>(a.res), trow + f, rr);
-        } else {
-#pragma unroll
-          for (int q = 0; q < 4; ++q) zz[q] = rr[q] = 0.f;
-        }
-#pragma unroll
-        for (int q = 0; q < 4; ++q) v[b][q] = acc[q] + zz[q] + rr[q];
+      for (int b = 0; b < FB; ++b) {
+        w0[b] = ld_frag(wu + (long)b * 16 * MB);
+        w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
       }
+    }
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mfma16(w0[b], g0, acc);
+      acc = mfma16(w1[b], g1, acc);
+      float zz[4];
+      St<bf16>::ld4(sZ, l16 * DP + f0 + b * 16 + 4 * grp, zz);
+      const float r4[4] = {__uint_as_float(rr[b].x << 16), __uint_as_float(rr[b].x & 0xffff0000u),
+                           __uint_as_float(rr[b].y << 16), __uint_as_float(rr[b].y & 0xffff0000u)};
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[b][q] = acc[q] + zz[q] + r4[q];
     }
   }
 
   auto row_sum = [&](float s) {  // sum over the token's features across the workgroup
     s += __shfl_xor(s, 16, 64);
     s += __shfl_xor(s, 32, 64);
-    if (grp == 0) sRed[wave][l16] = s;
+    if (grp == 0) sRed[wave * TOK + l16] = s;
     __syncthreads();
     float t = 0.f;
 #pragma unroll
-    for (int w = 0; w < NW; ++w) t += sRed[w][l16];
+    for (int w = 0; w < NW; ++w) t += sRed[w * TOK + l16];
     __syncthreads();
     return t;
   };
@@ -105,73 +158,66 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   if (a.norm == Norm::None) {
     if (tv)
 #pragma unroll
-      for (int b = 0; b < 16; ++b)
-        if (b < FB) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
+      for (int b = 0; b < FB; ++b) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
     return;
   }
-  const float inv_d = 1.f / (float)d;
+  constexpr float inv_d = 1.f / (float)D;
   float mean = 0.f;
   if (a.norm == Norm::LN) {
     float s = 0.f;
 #pragma unroll
-    for (int b = 0; b < 16; ++b)
-      if (b < FB)
+    for (int b = 0; b < FB; ++b)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) s += v[b][q];
+      for (int q = 0; q < 4; ++q) s += v[b][q];
     mean = row_sum(s) * inv_d;
   } else if (tv) {
 #pragma unroll
-    for (int b = 0; b < 16; ++b)  // RMS: the residual stream h itself is an output
-      if (b < FB) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
+    for (int b = 0; b < FB; ++b)  // RMS: the residual stream h itself is an output
+      St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
   }
   float s2 = 0.f;
 #pragma unroll
-  for (int b = 0; b < 16; ++b)
-    if (b < FB)
+  for (int b = 0; b < FB; ++b)
 #pragma unroll
-      for (int q = 0; q < 4; ++q) {
-        const float c = v[b][q] - mean;
-        s2 += c * c;
-      }
+    for (int q = 0; q < 4; ++q) {
+      const float c = v[b][q] - mean;
+      s2 += c * c;
+    }
   const float rstd = rsqrtf(row_sum(s2) * inv_d + a.eps);
   if (!tv) return;
   if (a.rstd && wave == 0 && grp == 0) a.rstd[token] = rstd;
   bf16* out = static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm);
 #pragma unroll
-  for (int b = 0; b < 16; ++b) {
-    if (b < FB) {
-      const int f = f0 + b * 16 + 4 * grp;
-      float xh[4], gm[4], bt[4], o[4];
+  for (int b = 0; b < FB; ++b) {
+    const int f = f0 + b * 16 + 4 * grp;
+    float xh[4], gm[4], bt[4] = {0.f, 0.f, 0.f, 0.f}, o[4];
 #pragma unroll
-      for (int q = 0; q < 4; ++q) xh[q] = (v[b][q] - mean) * rstd;
-      St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
-      if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
-      else
+    for (int q = 0; q < 4; ++q) xh[q] = (v[b][q] - mean) * rstd;
+    St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
+    if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
 #pragma unroll
-        for (int q = 0; q < 4; ++q) bt[q] = 0.f;
-#pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
-      St<bf16>::st4(out, trow + f, o);
-      if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), trow + f, xh);
-    }
+    for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
+    St<bf16>::st4(out, trow + f, o);
+    if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), trow + f, xh);
   }
 }
 
 // ================================================================ bf16 backward
-template <int NW>
+template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int KS = NW / 4;
+  constexpr int D = 16 * NW * FB, DP = D + 8, SLICE = D / KS;
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  const int d = a.d, T = a.T, DP = d + 8;
-  bf16* sdZ = reinterpret_cast<bf16*>(smem);                       // [TOK][d + 8]
+  bf16* sdZ = reinterpret_cast<bf16*>(smem);                       // [TOK][DP]
   bf16* sdU = sdZ + TOK * DP;                                      // [TOK][GP]
   float* sPart = reinterpret_cast<float*>(sdU + TOK * GP);         // [KS][TOK][MB]
   float* sRed = sPart + KS * TOK * MB;                             // [NW][TOK]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int T = a.T;
   const int token = blockIdx.x * TOK + l16;
   const bool tv = token < T;
-  const long trow = (long)(tv ? token : 0) * d;
-  const int FW = d / NW, FB = FW / 16, f0 = wave * FW;
+  const long trow = (long)(tv ? token : 0) * D;
+  const int f0 = wave * 16 * FB;
 
   auto row_sum = [&](float s) {
     s += __shfl_xor(s, 16, 64);
@@ -185,74 +231,100 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     return t;
   };
 
-  // ---- gradient at the adapter output
-  float dz[16][4];
+  // fragments of W_up for the first contraction: in flight during the norm backward
+  const int ug = wave % 4, ks = wave / 4;
+  constexpr int NSTEP = SLICE / 32;
+  constexpr bool PRE = FB <= 4;  // early loads while the registers allow
+  constexpr int NPRE = PRE ? NSTEP : 1;
+  bf16x8 wup_f[NPRE];
+  const bf16* wu = static_cast<const bf16*>(a.wup) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
+  if constexpr (PRE) {
+#pragma unroll
+    for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(wu + j * 32);
+  }
+
+  // ---- gradient at the adapter output (all loads issued up front)
+  float dz[FB][4];
   {
-    float gg[16][4], xh[16][4];
-    float s1 = 0.f, s2 = 0.f;
+    float gg[FB][4], xh[FB][4], dr[FB][4];
 #pragma unroll
-    for (int b = 0; b < 16; ++b) {
-      if (b < FB) {
-        const int f = f0 + b * 16 + 4 * grp;
-        if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.gin), trow + f, gg[b]);
-        else
+    for (int b = 0; b < FB; ++b) {
+      const long o = trow + f0 + b * 16 + 4 * grp;
 #pragma unroll
-          for (int q = 0; q < 4; ++q) gg[b][q] = 0.f;
-        if (a.norm != Norm::None) {
-          float gm[4];
-          St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
-          if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), trow + f, xh[b]);
-          else
-#pragma unroll
-            for (int q = 0; q < 4; ++q) xh[b][q] = 0.f;
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            gg[b][q] *= gm[q];
-            s1 += gg[b][q];
-            s2 += gg[b][q] * xh[b][q];
-          }
-        }
+      for (int q = 0; q < 4; ++q) gg[b][q] = xh[b][q] = dr[b][q] = 0.f;
+      if (tv) {
+        St<bf16>::ld4(static_cast<const bf16*>(a.gin), o, gg[b]);
+        if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), o, xh[b]);
+        if (a.norm == Norm::RMS) St<bf16>::ld4(static_cast<const bf16*>(a.dres), o, dr[b]);
       }
     }
+    const float rs = (tv && a.norm != Norm::None) ? a.rstd[token] : 0.f;
     if (a.norm == Norm::None) {
 #pragma unroll
-      for (int b = 0; b < 16; ++b)
+      for (int b = 0; b < FB; ++b)
 #pragma unroll
         for (int q = 0; q < 4; ++q) dz[b][q] = gg[b][q];
     } else {
-      const float inv_d = 1.f / (float)d;
-      const float m1 = (a.norm == Norm::LN) ? row_sum(s1) * inv_d : 0.f;
-      const float m2 = row_sum(s2) * inv_d;
-      const float rs = tv ? a.rstd[token] : 0.f;
+      float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int b = 0; b < 16; ++b) {
-        if (b < FB) {
-          float dr[4] = {0.f, 0.f, 0.f, 0.f};
-          if (a.norm == Norm::RMS && tv)
-            St<bf16>::ld4(static_cast<const bf16*>(a.dres), trow + f0 + b * 16 + 4 * grp, dr);
+      for (int b = 0; b < FB; ++b) {
+        float gm[4];
+        St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f0 + b * 16 + 4 * grp, gm);
 #pragma unroll
-          for (int q = 0; q < 4; ++q) dz[b][q] = dr[q] + rs * (gg[b][q] - m1 - xh[b][q] * m2);
+        for (int q = 0; q < 4; ++q) {
+          gg[b][q] *= gm[q];
+          s1 += gg[b][q];
+          s2 += gg[b][q] * xh[b][q];
         }
       }
+      constexpr float inv_d = 1.f / (float)D;
+      const float m1 = (a.norm == Norm::LN) ? row_sum(s1) * inv_d : 0.f;
+      const float m2 = row_sum(s2) * inv_d;
+#pragma unroll
+      for (int b = 0; b < FB; ++b)
+#pragma unroll
+        for (int q = 0; q < 4; ++q) dz[b][q] = dr[b][q] + rs * (gg[b][q] - m1 - xh[b][q] * m2);
     }
   }
 #pragma unroll
-  for (int b = 0; b < 16; ++b) {
-    if (b < FB) {
-      const int f = f0 + b * 16 + 4 * grp;
-      if (tv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), trow + f, dz[b]);
-      St<bf16>::st4(sdZ, (long)l16 * DP + f, dz[b]);
+  for (int b = 0; b < FB; ++b) {
+    const int f = f0 + b * 16 + 4 * grp;
+    if (tv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), trow + f, dz[b]);
+    St<bf16>::st4(sdZ, (long)l16 * DP + f, dz[b]);
+  }
+  // W_down fragments of the last contraction, in flight during the dV one
+  bf16x8 w0[FB], w1[FB];
+  const bf16* wd = static_cast<const bf16*>(a.wdn) + (long)(f0 + l16) * MB + 8 * grp;
+  if (PRE && a.dzin) {
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      w0[b] = ld_frag(wd + (long)b * 16 * MB);
+      w1[b] = ld_frag(wd + (long)b * 16 * MB + 32);
     }
   }
   __syncthreads();
 
   // ---- dV^T[unit][token] = W_up[unit][:] . dZ[token][:]; dU = dV * gelu'(U)
   {
-    const int ug = wave % 4, ks = wave / 4, slice = d / KS;
-    const bf16* wu = static_cast<const bf16*>(a.wup) + (long)(ug * 16 + l16) * d + 8 * grp;
-    const bf16* zr = sdZ + l16 * DP + 8 * grp;
+    const bf16* zr = sdZ + l16 * DP + ks * SLICE + 8 * grp;
+    const int j0 = ug * 16 + 4 * grp;
+    float uu[4] = {0.f, 0.f, 0.f, 0.f};
+    if (tv && ks == 0) St<bf16>::ld4(static_cast<const bf16*>(a.u), (long)token * MB + j0, uu);
     f32x4 dv = {0.f, 0.f, 0.f, 0.f};
-    for (int kk = ks * slice; kk < (ks + 1) * slice; kk += 32) dv = mfma16(ld_frag(wu + kk), ld_frag(zr + kk), dv);
+    if constexpr (PRE) {
+#pragma unroll
+      for (int j = 0; j < NSTEP; ++j) dv = mfma16(wup_f[j], ld_frag(zr + j * 32), dv);
+    } else {
+      constexpr int RUN = NSTEP < 8 ? NSTEP : 8;
+#pragma unroll
+      for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
+        bf16x8 w[RUN];
+#pragma unroll
+        for (int j = 0; j < RUN; ++j) w[j] = ld_frag(wu + (k0 + j) * 32);
+#pragma unroll
+        for (int j = 0; j < RUN; ++j) dv = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), dv);
+      }
+    }
     if constexpr (KS > 1) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) sPart[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = dv[r];
@@ -268,9 +340,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
       }
     }
     if (ks == 0) {
-      const int j0 = ug * 16 + 4 * grp;
-      float uu[4] = {0.f, 0.f, 0.f, 0.f}, du[4];
-      if (tv) St<bf16>::ld4(static_cast<const bf16*>(a.u), (long)token * MB + j0, uu);
+      float du[4];
 #pragma unroll
       for (int r = 0; r < 4; ++r) du[r] = dv[r] * gelu_grad_f(uu[r]);
       if (tv) St<bf16>::st4(static_cast<bf16*>(a.du), (long)token * MB + j0, du);
@@ -281,29 +351,36 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   __syncthreads();
 
   // ---- dzin^T[f][token] = dZ + W_down[f][:] . dU[token][:]
-  const bf16* wd = static_cast<const bf16*>(a.wdn) + (long)(f0 + l16) * MB + 8 * grp;
   const bf16x8 u0 = ld_frag(sdU + l16 * GP + 8 * grp), u1 = ld_frag(sdU + l16 * GP + 32 + 8 * grp);
+  if constexpr (!PRE) {
 #pragma unroll
-  for (int b = 0; b < 16; ++b) {
-    if (b < FB) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = mfma16(ld_frag(wd + (long)b * 16 * MB), u0, acc);
-      acc = mfma16(ld_frag(wd + (long)b * 16 * MB + 32), u1, acc);
-      float o[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) o[q] = dz[b][q] + acc[q];
-      if (tv) St<bf16>::st4(static_cast<bf16*>(a.dzin), trow + f0 + b * 16 + 4 * grp, o);
+    for (int b = 0; b < FB; ++b) {
+      w0[b] = ld_frag(wd + (long)b * 16 * MB);
+      w1[b] = ld_frag(wd + (long)b * 16 * MB + 32);
     }
+  }
+#pragma unroll
+  for (int b = 0; b < FB; ++b) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mfma16(w0[b], u0, acc);
+    acc = mfma16(w1[b], u1, acc);
+    float o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = dz[b][q] + acc[q];
+    if (tv) St<bf16>::st4(static_cast<bf16*>(a.dzin), trow + f0 + b * 16 + 4 * grp, o);
   }
 }
 
 // ================================================================ bf16 weight gradients
 // C[p][q] += sum_t X[t][p] * Y[t][q]: blockIdx.z = 0 -> dW_up (X = gelu(U), Y = dZ),
-// 1 -> dW_down (X = z, Y = dU).  64x64 output tiles, 256 tokens per workgroup.
+// 1 -> dW_down (X = z, Y = dU).  64x64 output tiles, DW_TC tokens per
+// workgroup.  Token-major tiles go to LDS as they are in memory (16-B chunks);
+// the MFMA operands, which need 8 consecutive tokens per lane, are read with
+// the LDS transpose read.
 constexpr int DW_TC = 256;
 __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
-  __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [p][token]
-  __shared__ __attribute__((aligned(16))) bf16 sY[64 * GP];  // [q][token]
+  __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [token][p]
+  __shared__ __attribute__((aligned(16))) bf16 sY[64 * GP];  // [token][q]
   const bool up = blockIdx.z == 0;
   const int d = a.d, T = a.T;
   const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
@@ -318,33 +395,40 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
   const int tbeg = blockIdx.y * DW_TC, tend = min(T, tbeg + DW_TC);
-  for (int t0 = tbeg; t0 < tend; t0 += 64) {
+  constexpr int NSUB = DW_TC / 64;
+  // every 16-B chunk of the chunk's X and Y rows, loaded before the first use
+  bf16x8 xr[NSUB][2], yr[NSUB][2];
+#pragma unroll
+  for (int sb = 0; sb < NSUB; ++sb)
+#pragma unroll
+    for (int i = 0; i < 2; ++i) {
+      const int idx = tid + i * 256, tt = idx / 8, c = idx % 8, t = tbeg + sb * 64 + tt;
+      xr[sb][i] = t < tend ? ld_frag(X + (long)t * ldx + p0 + c * 8) : zero_frag();
+      yr[sb][i] = t < tend ? ld_frag(Y + (long)t * ldy + q0 + c * 8) : zero_frag();
+    }
+#pragma unroll
+  for (int sb = 0; sb < NSUB; ++sb) {
+    if (tbeg + sb * 64 >= tend) break;
     __syncthreads();
 #pragma unroll
-    for (int i = 0; i < 2; ++i) {  // 64 tokens x 8 chunks of 8 columns, for X and Y
-      const int idx = tid + i * 256, tt = idx / 8, c = idx % 8, t = t0 + tt;
-      float xv[8], yv[8];
-      if (t < tend) {
-        unpack_frag(ld_frag(X + (long)t * ldx + p0 + c * 8), xv);
-        unpack_frag(ld_frag(Y + (long)t * ldy + q0 + c * 8), yv);
-        if (up)
+    for (int i = 0; i < 2; ++i) {
+      const int idx = tid + i * 256, tt = idx / 8, c = idx % 8;
+      bf16x8 xv = xr[sb][i];
+      if (up) {
+        float f[8];
+        unpack_frag(xv, f);
 #pragma unroll
-          for (int v = 0; v < 8; ++v) xv[v] = gelu_f(xv[v]);
-      } else {
-#pragma unroll
-        for (int v = 0; v < 8; ++v) xv[v] = yv[v] = 0.f;
+        for (int v = 0; v < 8; ++v) f[v] = gelu_f(f[v]);
+        xv = pack_frag(f);
       }
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        sX[(c * 8 + v) * GP + tt] = f2bf(xv[v]);
-        sY[(c * 8 + v) * GP + tt] = f2bf(yv[v]);
-      }
+      *reinterpret_cast<bf16x8*>(sX + tt * GP + c * 8) = xv;
+      *reinterpret_cast<bf16x8*>(sY + tt * GP + c * 8) = yr[sb][i];
     }
     __syncthreads();
 #pragma unroll
     for (int ks = 0; ks < 4; ++ks)
-      acc = mfma32(ld_frag(sX + (wp * 32 + l32) * GP + ks * 16 + 8 * half),
-                   ld_frag(sY + (wq * 32 + l32) * GP + ks * 16 + 8 * half), acc);
+      acc = mfma32(lds_tr_frag32(sX, GP, ks * 16, wp * 32, lane), lds_tr_frag32(sY, GP, ks * 16, wq * 32, lane),
+                   acc);
   }
   // D[i = p][j = q]: lane holds q = wq*32 + l32, p = wp*32 + 8*(r/4) + 4*half + r%4
 #pragma unroll
@@ -493,10 +577,42 @@ __global__ __launch_bounds__(256) void adapter_dw_f32(AdapterDwArgs a) {
 // ================================================================ launchers
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
-static int bf16_waves(int d) {  // waves per row-kernel workgroup, 0 if unsupported
-  if (d % 64 == 0 && d <= 1024) return 4;
-  if (d % 256 == 0 && d <= 4096) return 16;
-  return 0;
+// bf16 row kernels: (waves, feature blocks per wave) for a model width
+static bool bf16_shape(int d, int& nw, int& fb) {
+  // 16 waves (4 per SIMD) per 16-token workgroup: d = 256 * fb
+  if (d % 256 == 0 && d <= 4096) { nw = 16; fb = d / 256; return true; }
+  return false;
+}
+
+template <int NW, int FB>
+static hipError_t fwd_k(const AdapterFwdArgs& a, hipStream_t s) {
+  constexpr int D = 16 * NW * FB;
+  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
+                    (size_t)NW * TOK * 4;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_fwd_bf16<NW, FB>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)sh);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL((adapter_fwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
+  return hipGetLastError();
+}
+template <int NW, int FB>
+static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
+  constexpr int D = 16 * NW * FB;
+  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
+                    (size_t)NW * TOK * 4;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_bwd_bf16<NW, FB>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)sh);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL((adapter_bwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
+  return hipGetLastError();
 }
 
 hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s) {
@@ -507,12 +623,19 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
   if (a.norm == Norm::RMS && !a.out_norm) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
   if (dtype == DT_BF16) {
-    const int nw = bf16_waves(a.d);
-    if (!nw || a.m != MB || !al16(a.z) || !al16(a.wdn_t) || !al16(a.wup_t)) return hipErrorInvalidValue;
-    const dim3 grid((a.T + TOK - 1) / TOK);
-    if (nw == 4) hipLaunchKernelGGL(adapter_fwd_bf16<4>, grid, dim3(256), 0, s, a);
-    else hipLaunchKernelGGL(adapter_fwd_bf16<16>, grid, dim3(1024), 0, s, a);
-    return hipGetLastError();
+    int nw, fb;
+    if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.z) || !al16(a.wdn_t) || !al16(a.wup_t))
+      return hipErrorInvalidValue;
+    switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
+      case 1: return fwd_k<16, 1>(a, s);
+      case 2: return fwd_k<16, 2>(a, s);
+      case 3: return fwd_k<16, 3>(a, s);
+      case 4: return fwd_k<16, 4>(a, s);
+      case 8: return fwd_k<16, 8>(a, s);
+      case 12: return fwd_k<16, 12>(a, s);
+      case 16: return fwd_k<16, 16>(a, s);
+    }
+    return hipErrorInvalidValue;
   }
   const size_t sh = (2 * (size_t)a.d + a.m + 8) * sizeof(float);
   if (sh > 64 * 1024) return hipErrorInvalidValue;
@@ -528,14 +651,18 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
   if (a.norm == Norm::RMS && !a.dres) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
   if (dtype == DT_BF16) {
-    const int nw = bf16_waves(a.d);
-    if (!nw || a.m != MB || !al16(a.wup) || !al16(a.wdn)) return hipErrorInvalidValue;
-    const size_t sh = (size_t)TOK * (a.d + 8) * 2 + (size_t)TOK * GP * 2 +
-                      (size_t)(nw / 4) * TOK * MB * 4 + (size_t)nw * TOK * 4;
-    const dim3 grid((a.T + TOK - 1) / TOK);
-    if (nw == 4) hipLaunchKernelGGL(adapter_bwd_bf16<4>, grid, dim3(256), sh, s, a);
-    else hipLaunchKernelGGL(adapter_bwd_bf16<16>, grid, dim3(1024), sh, s, a);
-    return hipGetLastError();
+    int nw, fb;
+    if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.wup) || !al16(a.wdn)) return hipErrorInvalidValue;
+    switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
+      case 1: return bwd_k<16, 1>(a, s);
+      case 2: return bwd_k<16, 2>(a, s);
+      case 3: return bwd_k<16, 3>(a, s);
+      case 4: return bwd_k<16, 4>(a, s);
+      case 8: return bwd_k<16, 8>(a, s);
+      case 12: return bwd_k<16, 12>(a, s);
+      case 16: return bwd_k<16, 16>(a, s);
+    }
+    return hipErrorInvalidValue;
   }
   const size_t sh = ((size_t)a.d + a.m + 8) * sizeof(float);
   if (sh > 64 * 1024) return hipErrorInvalidValue;

@@ -10,7 +10,8 @@
 // softmax row statistics are mostly in-lane.  The probabilities are fed back
 // to the second MFMA straight from registers: within one 16-wide k step the
 // lane's values cover 16 keys in a fixed permuted order, and the other operand
-// is read from a transposed LDS tile in that same order.
+// is read in that same order from the row-major LDS tile with the gfx950 LDS
+// transpose read (ds_read_b64_tr_b16), so no tile is ever stored transposed.
 //
 // Log-sum-exp is kept in base 2 of the scaled scores: lse2 = log2 sum_j
 // 2^(s_j * scale * log2 e).
@@ -28,17 +29,19 @@ __device__ __forceinline__ void rope_cs(int pos, int i, int dh, float log2theta,
 
 // ================================================================ bf16 / MFMA
 constexpr int KT = 64;       // keys (or queries) per LDS tile
-constexpr int TP = KT + 8;   // pitch of transposed tiles [dim][KT]
 
 // Loads a [KT x DH] tile of rows r0.. (rows >= S are zero) from the Q/K/V
-// column block `col` into LDS row-major (pitch DH + 8) and/or transposed
-// (pitch TP), rotating pairs (i, i + DH/2) when rot.
+// column block `col` into LDS row-major (pitch DH + 8), rotating pairs
+// (i, i + DH/2) when rot.
 template <int DH>
 __device__ __forceinline__ void load_tile(const bf16* qkv, int ld, int b, int S, int r0, int col,
-                                          bool rot, float log2theta, bf16* rowmaj, bf16* trans) {
+                                          bool rot, float log2theta, bf16* rowmaj) {
   constexpr int HC = DH / 16;  // 8-element chunk pairs per row (chunk c with c + DH/16)
   constexpr int PAIRS = KT * HC;
-  for (int p = threadIdx.x; p < PAIRS; p += blockDim.x) {
+  static_assert(PAIRS % 256 == 0, "256-thread workgroups");
+#pragma unroll
+  for (int it = 0; it < PAIRS / 256; ++it) {
+    const int p = threadIdx.x + it * 256;
     const int r = p / HC, c = p % HC, row = r0 + r;
     float x1[8], x2[8];
     if (row < S) {
@@ -59,17 +62,8 @@ __device__ __forceinline__ void load_tile(const bf16* qkv, int ld, int b, int S,
 #pragma unroll
       for (int v = 0; v < 8; ++v) x1[v] = x2[v] = 0.f;
     }
-    if (rowmaj) {
-      *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8) = pack_frag(x1);
-      *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8 + DH / 2) = pack_frag(x2);
-    }
-    if (trans) {
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        trans[(c * 8 + v) * TP + r] = f2bf(x1[v]);
-        trans[(c * 8 + DH / 2 + v) * TP + r] = f2bf(x2[v]);
-      }
-    }
+    *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8) = pack_frag(x1);
+    *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8 + DH / 2) = pack_frag(x2);
   }
 }
 
@@ -102,14 +96,14 @@ __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool va
   for (int s = 0; s < DH / 16; ++s) f[s] = pack_frag(x[s]);
 }
 
-// A-operand fragment from a transposed tile: row `dimrow`, the 8 permuted
-// positions matching register values r = 8j..8j+7 of score block kb.
-__device__ __forceinline__ bf16x8 perm_frag(const bf16* trans, int dimrow, int kb, int j, int half) {
-  const bf16* p = trans + dimrow * TP + kb * 32 + 16 * j + 4 * half;
-  uint2 lo = *reinterpret_cast<const uint2*>(p);
-  uint2 hi = *reinterpret_cast<const uint2*>(p + 8);
-  uint4 q = make_uint4(lo.x, lo.y, hi.x, hi.y);
-  return __builtin_bit_cast(bf16x8, q);
+// A-operand fragment of (tile^T): rows = dims db*32 + lane%32 of a row-major
+// [row][dim] LDS tile, k = the 8 permuted rows matching register values
+// r = 8j..8j+7 of score block kb (rows kb*32 + 16j + 4*half + {0..3, 8..11}).
+template <int DH>
+__device__ __forceinline__ bf16x8 perm_frag(const bf16* tile, int db, int kb, int j, int lane) {
+  const int g = lane >> 4, dims = db * 32 + 16 * (g & 1), rows = kb * 32 + 16 * j + 4 * (g >> 1);
+  const uint2 lo = lds_tr4(tile, DH + 8, rows, dims, lane), hi = lds_tr4(tile, DH + 8, rows + 8, dims, lane);
+  return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
 }
 
 __device__ __forceinline__ bf16x8 pack8(const f32x16& v, int j) {
@@ -154,7 +148,7 @@ __device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, 
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sVt[DH * TP];
+  __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
   const int q = blockIdx.x * 128 + wave * 32 + l32;
@@ -179,8 +173,8 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK, nullptr);
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, nullptr, sVt);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
     __syncthreads();
     f32x16 sc[2];
 #pragma unroll
@@ -226,7 +220,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
         const bf16x8 pf = pack8(sc[kb], j);
 #pragma unroll
         for (int db = 0; db < DH / 32; ++db)
-          oacc[db] = mfma32(perm_frag(sVt, db * 32 + l32, kb, j, half), pf, oacc[db]);
+          oacc[db] = mfma32(perm_frag<DH>(sV, db, kb, j, lane), pf, oacc[db]);
       }
   }
   if (qv) {
@@ -240,7 +234,6 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sKt[DH * TP];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
@@ -284,8 +277,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK, sKt);
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV, nullptr);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
     __syncthreads();
 #pragma unroll
     for (int kb = 0; kb < 2; ++kb) {
@@ -309,7 +302,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
         const bf16x8 sf = pack8(st, j);
 #pragma unroll
         for (int db = 0; db < DH / 32; ++db)
-          dq[db] = mfma32(perm_frag(sKt, db * 32 + l32, kb, j, half), sf, dq[db]);
+          dq[db] = mfma32(perm_frag<DH>(sK, db, kb, j, lane), sf, dq[db]);
       }
     }
   }
@@ -323,9 +316,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
 template <int DH, bool CAUSAL>
 __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sQ[KT * (DH + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sQt[DH * TP];
   __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
-  __shared__ __attribute__((aligned(16))) bf16 sOt[DH * TP];
   __shared__ float sL[KT], sD[KT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
@@ -352,8 +343,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
   const int qt0 = CAUSAL ? (blockIdx.x * 128) / KT : 0;
   for (int qt = qt0; qt < nqt; ++qt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ, sQt);
-    load_tile<DH>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO, sOt);
+    load_tile<DH>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ);
+    load_tile<DH>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
       sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
@@ -384,8 +375,8 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
         const bf16x8 pf = pack8(st, j), sf = pack8(ds, j);
 #pragma unroll
         for (int db = 0; db < DH / 32; ++db) {
-          dv[db] = mfma32(perm_frag(sOt, db * 32 + l32, qb, j, half), pf, dv[db]);
-          dk[db] = mfma32(perm_frag(sQt, db * 32 + l32, qb, j, half), sf, dk[db]);
+          dv[db] = mfma32(perm_frag<DH>(sO, db, qb, j, lane), pf, dv[db]);
+          dk[db] = mfma32(perm_frag<DH>(sQ, db, qb, j, lane), sf, dk[db]);
         }
       }
     }

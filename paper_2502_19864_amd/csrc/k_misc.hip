@@ -204,7 +204,9 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
   return hipGetLastError();
 }
 
-// workgroup 0: the head over every sample; the others zero dy outside position 0
+// Workgroup 0 runs the head: wave w takes samples w, w + 4, ...; each lane
+// holds features lane + 64 j, so every per-sample reduction is a wave
+// shuffle.  The other workgroups zero dy outside position 0.
 template <typename T>
 __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
                                                  const float* bh, int C, const int* labels, T* dy,
@@ -217,40 +219,42 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
     }
     return;
   }
-  __shared__ float red[4];
-  __shared__ float sl[16];
+  __shared__ float sloss[4];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float total = 0.f;
-  for (int b = 0; b < B; ++b) {
+  for (int b = wave; b < B; b += 4) {
     const long row = (long)b * S * d;
-    for (int c = 0; c < C; ++c) {
-      float p = 0.f;
-      for (int i = threadIdx.x; i < d; i += blockDim.x) p += St<T>::ld(y, row + i) * wh[(long)i * C + c];
-      p = blk_sum<T>(p, red);
-      if (threadIdx.x == 0) sl[c] = p + bh[c];
+    float lg[16];
+    for (int c = 0; c < C; ++c) lg[c] = 0.f;
+    for (int i = lane; i < d; i += 64) {
+      const float yi = St<T>::ld(y, row + i);
+      for (int c = 0; c < C; ++c) lg[c] += yi * wh[(long)i * C + c];
     }
-    __syncthreads();
     float mx = -INFINITY;
-    for (int c = 0; c < C; ++c) mx = fmaxf(mx, sl[c]);
+    for (int c = 0; c < C; ++c) {
+      lg[c] = wave_sum(lg[c]) + bh[c];
+      mx = fmaxf(mx, lg[c]);
+    }
     float se = 0.f;
-    for (int c = 0; c < C; ++c) se += __expf(sl[c] - mx);
+    for (int c = 0; c < C; ++c) se += __expf(lg[c] - mx);
     const int lab = labels[b];
-    total += -(sl[lab] - mx - __logf(se));
+    total += -(lg[lab] - mx - __logf(se));
     float dl[16];
-    for (int c = 0; c < C; ++c) dl[c] = (__expf(sl[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
-    for (int i = threadIdx.x; i < d; i += blockDim.x) {
+    for (int c = 0; c < C; ++c) dl[c] = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
+    for (int i = lane; i < d; i += 64) {
       const float yi = St<T>::ld(y, row + i);
       float g = 0.f;
       for (int c = 0; c < C; ++c) {
         g += dl[c] * wh[(long)i * C + c];
-        gwh[(long)i * C + c] += yi * dl[c];
+        atomicAdd(gwh + (long)i * C + c, yi * dl[c]);
       }
       St<T>::st(dy, row + i, g);
     }
-    if (threadIdx.x == 0)
-      for (int c = 0; c < C; ++c) gbh[c] += dl[c];
-    __syncthreads();
+    if (lane < C) atomicAdd(gbh + lane, dl[lane]);
   }
-  if (loss && threadIdx.x == 0) *loss = total / (float)B;
+  if (lane == 0) sloss[wave] = total;
+  __syncthreads();
+  if (loss && threadIdx.x == 0) *loss = (sloss[0] + sloss[1] + sloss[2] + sloss[3]) / (float)B;
 }
 
 hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const float* wh, const float* bh,

@@ -159,9 +159,9 @@ static ringada_status check_desc(const ringada_stage_desc* D) {
   if (D->arch == RINGADA_ARCH_PRERMS_SWIGLU && !(D->rope_theta > 0.f))
     return fail(RINGADA_E_INVALID, "rope_theta must be > 0");
   if (D->dtype == RINGADA_BF16) {
-    if (D->d_model % 64 || D->d_model > 4096 || (D->d_model > 1024 && D->d_model % 256))
-      return fail(RINGADA_E_UNSUPPORTED, "bf16 path: d_model must be a multiple of 64 up to 1024, "
-                                         "or of 256 up to 4096 (got %d)", D->d_model);
+    if (D->d_model % 256 || D->d_model > 4096 || (D->d_model > 1024 && D->d_model % 1024))
+      return fail(RINGADA_E_UNSUPPORTED, "bf16 path: d_model must be a multiple of 256 up to 1024, "
+                                         "or of 1024 up to 4096 (got %d)", D->d_model);
     if (dh != 64 && dh != 128)
       return fail(RINGADA_E_UNSUPPORTED, "bf16 path: head dim must be 64 or 128 (got %d)", dh);
     if (D->d_ffn % 64) return fail(RINGADA_E_UNSUPPORTED, "bf16 path: d_ffn must be a multiple of 64");

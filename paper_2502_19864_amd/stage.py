@@ -41,7 +41,6 @@ class Stage:
         self.dev = torch.device("cuda", device)
         self.sdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.desc = make_desc(w, max_batch, max_seq)
-        self.stream = torch.cuda.current_stream(self.dev)
         self.handle = B.ringada_stage_create(self.desc)
         self.frozen = []
         self.adapters = []
@@ -66,7 +65,9 @@ class Stage:
     # ------------------------------------------------------------ helpers
     @property
     def sptr(self):
-        return self.stream.cuda_stream
+        """The current torch stream of the device (calls are stream-ordered on
+        it, so they can also be captured into a HIP graph)."""
+        return self.torch.cuda.current_stream(self.dev).cuda_stream
 
     def upload(self, a):
         """float32 numpy (bf16-representable for bf16 stages) -> device tensor in the storage dtype."""
