@@ -10,8 +10,10 @@ update of the unfrozen adapters.  Prints one JSON line.
 from __future__ import annotations
 
 import argparse
+import hashlib
 import json
 import os
+import re
 import sys
 import time
 
@@ -24,6 +26,51 @@ METRIC = "stage fine-tune samples/sec (fwd+early-stop bwd); % bf16 MFMA peak"
 PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA, published
 PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
 GEMM_PREFIX = "gemm_"
+CSRC = os.path.join(ROOT, "paper_2502_19864_amd", "csrc")
+# source files that define each family of named kernels
+KERNEL_SOURCES = {"gemm_": ("k_gemm.hip", "common.h", "kernels.h"),
+                  "attn_": ("k_attention.hip", "common.h", "kernels.h"),
+                  "adapter_": ("k_adapter.hip", "k_misc.hip", "common.h", "kernels.h")}
+
+
+def kernel_source_hash(name):
+    """sha256 over the sources that define the kernel family of `name`."""
+    files = next((f for pre, f in KERNEL_SOURCES.items() if name.startswith(pre)), None)
+    if files is None:
+        return None
+    h = hashlib.sha256()
+    for f in files:
+        with open(os.path.join(CSRC, f), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def recorded_traffic(name, workload):
+    """HBM bytes per launch of kernel `name` on `workload`, from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE summary, if one exists and was taken on
+    the current sources of that kernel; else None."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    want = kernel_source_hash(name)
+    for line in open(path):
+        m = re.match(r"\s*traffic:\s+kernel=(\S+)\s+bytes_per_launch=(\d+)\s+source_sha256=([0-9a-f]+)", line)
+        if m and m.group(1) == name and m.group(3) == want:
+            return int(m.group(2))
+    return None
+
+
+def copy_calibration(torch, mib, reps=5):
+    """A plain elementwise copy (dst = -src, float32) of `mib` MiB read and
+    `mib` MiB written per launch: the known-size kernel that scales the
+    FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    n = mib * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        torch.neg(src, out=dst)
+    torch.cuda.synchronize()
+    log(f"[bench] copy calibration: {reps} launches of neg() over {mib} MiB float32 in, {mib} MiB out")
 
 
 def log(*a):
@@ -66,6 +113,8 @@ def main():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-graph", action="store_true",
                     help="launch every kernel from the host each step instead of replaying a HIP graph")
+    ap.add_argument("--copy-calib-mib", type=int, default=0,
+                    help="after the bench, run a plain copy kernel of this many MiB (counter calibration)")
     args = ap.parse_args()
     if args.gpus != 1:
         print(f"bench.py: this build runs one ring stage on one GPU; --gpus {args.gpus} is not supported "
@@ -179,8 +228,11 @@ def main():
                 "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4), "traffic": None,
                 "avg_us": round(dom_avg_s * 1e6, 2), "launches_per_step": dom["launches"] // args.steps}
 
+    roof["traffic"] = recorded_traffic(dom["name"], w.name)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, inp)
     st.close()
+    if args.copy_calib_mib:
+        copy_calibration(torch, args.copy_calib_mib)
     out = {
         "metric": METRIC, "value": round(value, 2), "unit": "samples/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",

@@ -204,65 +204,122 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
   return hipGetLastError();
 }
 
-// Workgroup 0 runs the head: wave w takes samples w, w + 4, ...; each lane
-// holds features lane + 64 j, so every per-sample reduction is a wave
-// shuffle.  The other workgroups zero dy outside position 0.
+// Initiator's classification head on the [CLS] (position 0) token of each
+// sample: logits = y[b, 0, :] W_h + b_h, mean cross-entropy over the batch,
+// dy[b, 0, :] = dlogits W_h^T and zero at every other position, and the head
+// gradients accumulated into gwh / gbh.  Workgroup 0 does the head in two
+// phases per chunk of HEAD_CHUNK samples: (1) one wave per sample computes the
+// logits and dlogits into LDS, (2) one thread per feature i accumulates
+// gwh[i, :] over the chunk and writes dy[b, 0, i].  It alone owns gwh / gbh /
+// loss, so no atomics are needed.  The other workgroups zero the rows of dy
+// at positions 1..S-1.
+constexpr int HEAD_C = 16;      // maximum number of classes
+constexpr int HEAD_CHUNK = 64;  // samples per LDS chunk
 template <typename T>
 __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
                                                  const float* bh, int C, const int* labels, T* dy,
                                                  float* gwh, float* gbh, float* loss) {
   if (blockIdx.x > 0) {
-    const long per = (long)(S - 1) * d, n = (long)B * per;
-    for (long i = (long)(blockIdx.x - 1) * blockDim.x + threadIdx.x; i < n; i += (long)(gridDim.x - 1) * blockDim.x) {
-      const long b = i / per, r = i % per;
-      St<T>::st(dy, b * S * d + d + r, 0.f);
+    const int nz = gridDim.x - 1;
+    for (int r = blockIdx.x - 1; r < B * S; r += nz) {
+      if (r % S == 0) continue;
+      T* row = dy + (long)r * d;
+      for (int i = threadIdx.x; i < d; i += 256) St<T>::st(row, i, 0.f);
     }
     return;
   }
-  __shared__ float sloss[4];
+  __shared__ float sdl[HEAD_CHUNK][HEAD_C];
+  __shared__ float sloss[HEAD_CHUNK];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  float total = 0.f;
-  for (int b = wave; b < B; b += 4) {
-    const long row = (long)b * S * d;
-    float lg[16];
-    for (int c = 0; c < C; ++c) lg[c] = 0.f;
-    for (int i = lane; i < d; i += 64) {
-      const float yi = St<T>::ld(y, row + i);
-      for (int c = 0; c < C; ++c) lg[c] += yi * wh[(long)i * C + c];
-    }
-    float mx = -INFINITY;
-    for (int c = 0; c < C; ++c) {
-      lg[c] = wave_sum(lg[c]) + bh[c];
-      mx = fmaxf(mx, lg[c]);
-    }
-    float se = 0.f;
-    for (int c = 0; c < C; ++c) se += __expf(lg[c] - mx);
-    const int lab = labels[b];
-    total += -(lg[lab] - mx - __logf(se));
-    float dl[16];
-    for (int c = 0; c < C; ++c) dl[c] = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
-    for (int i = lane; i < d; i += 64) {
-      const float yi = St<T>::ld(y, row + i);
-      float g = 0.f;
-      for (int c = 0; c < C; ++c) {
-        g += dl[c] * wh[(long)i * C + c];
-        atomicAdd(gwh + (long)i * C + c, yi * dl[c]);
+  float total = 0.f;     // thread 0's running loss
+  float gb[HEAD_C];      // thread 0's running bias gradient
+#pragma unroll
+  for (int c = 0; c < HEAD_C; ++c) gb[c] = 0.f;
+  for (int b0 = 0; b0 < B; b0 += HEAD_CHUNK) {
+    const int nb = min(HEAD_CHUNK, B - b0);
+    // phase 1: logits and dlogits, one wave per sample
+    for (int j = wave; j < nb; j += 4) {
+      const T* row = y + (long)(b0 + j) * S * d;
+      float lg[HEAD_C];
+#pragma unroll
+      for (int c = 0; c < HEAD_C; ++c) lg[c] = 0.f;
+      for (int i = lane; i < d; i += 64) {
+        const float yi = St<T>::ld(row, i);
+#pragma unroll
+        for (int c = 0; c < HEAD_C; ++c)
+          if (c < C) lg[c] += yi * wh[(long)i * C + c];
       }
-      St<T>::st(dy, row + i, g);
+      float mx = -INFINITY;
+#pragma unroll
+      for (int c = 0; c < HEAD_C; ++c)
+        if (c < C) {
+          lg[c] = wave_sum(lg[c]) + bh[c];
+          mx = fmaxf(mx, lg[c]);
+        }
+      float se = 0.f, ll = 0.f;
+      const int lab = labels[b0 + j];
+#pragma unroll
+      for (int c = 0; c < HEAD_C; ++c)
+        if (c < C) {
+          se += __expf(lg[c] - mx);
+          if (c == lab) ll = lg[c];
+        }
+      if (lane == 0) {
+        sloss[j] = -(ll - mx - __logf(se));
+#pragma unroll
+        for (int c = 0; c < HEAD_C; ++c)
+          if (c < C) sdl[j][c] = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
+      }
     }
-    if (lane < C) atomicAdd(gbh + lane, dl[lane]);
+    __syncthreads();
+    // phase 2: one thread per feature
+    for (int i = threadIdx.x; i < d; i += 256) {
+      float w[HEAD_C], acc[HEAD_C];
+#pragma unroll
+      for (int c = 0; c < HEAD_C; ++c) {
+        w[c] = c < C ? wh[(long)i * C + c] : 0.f;
+        acc[c] = 0.f;
+      }
+      for (int j = 0; j < nb; ++j) {
+        const long at = (long)(b0 + j) * S * d + i;
+        const float yi = St<T>::ld(y, at);
+        float g = 0.f;
+#pragma unroll
+        for (int c = 0; c < HEAD_C; ++c)
+          if (c < C) {
+            acc[c] += yi * sdl[j][c];
+            g += sdl[j][c] * w[c];
+          }
+        St<T>::st(dy, at, g);
+      }
+#pragma unroll
+      for (int c = 0; c < HEAD_C; ++c)
+        if (c < C) gwh[(long)i * C + c] += acc[c];
+    }
+    if (threadIdx.x == 0)
+      for (int j = 0; j < nb; ++j) {
+        total += sloss[j];
+#pragma unroll
+        for (int c = 0; c < HEAD_C; ++c)
+          if (c < C) gb[c] += sdl[j][c];
+      }
+    __syncthreads();
   }
-  if (lane == 0) sloss[wave] = total;
-  __syncthreads();
-  if (loss && threadIdx.x == 0) *loss = (sloss[0] + sloss[1] + sloss[2] + sloss[3]) / (float)B;
+  if (threadIdx.x == 0) {
+#pragma unroll
+    for (int c = 0; c < HEAD_C; ++c)
+      if (c < C) gbh[c] += gb[c];
+    if (loss) *loss = total / (float)B;
+  }
 }
 
 hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const float* wh, const float* bh,
                           int C, const int* labels, void* dy, float* gwh, float* gbh, float* loss,
                           hipStream_t s) {
-  if (!y || !wh || !bh || !labels || !dy || !gwh || !gbh || B <= 0 || S <= 0 || d <= 0 || C < 1 || C > 16)
+  if (!y || !wh || !bh || !labels || !dy || !gwh || !gbh || B <= 0 || S <= 0 || d <= 0 || C < 1 || C > HEAD_C)
     return hipErrorInvalidValue;
-  const dim3 grid(S > 1 ? 1 + 512 : 1), block(256);
+  const long zero_rows = (long)B * (S - 1);
+  const dim3 grid(1 + (unsigned)(zero_rows < 1024 ? zero_rows : 1024)), block(256);
   if (dtype == DT_BF16)
     hipLaunchKernelGGL(head_ce_k<bf16>, grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
                        (bf16*)dy, gwh, gbh, loss);
