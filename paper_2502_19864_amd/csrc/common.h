@@ -62,6 +62,35 @@ __device__ __forceinline__ float gelu_grad_f(float u) {  // Phi(u) + u phi(u)
 }
 __device__ __forceinline__ float sigmoid_f(float u) { return 1.f / (1.f + __expf(-u)); }
 
+// Cheaper GELU for bf16 outputs: erf by the rational-times-Gaussian form of
+// Abramowitz & Stegun, Handbook of Mathematical Functions, formula 7.1.26
+// (absolute error <= 1.5e-7, far below bf16 resolution).  For z = u / sqrt(2)
+// the Gaussian factor exp(-z^2) = exp(-u^2 / 2) is the one gelu' needs, so
+// both come from one exponential.
+struct ErfGauss {
+  float erf_z;  // erf(u / sqrt 2)
+  float gauss;  // exp(-u^2 / 2)
+};
+__device__ __forceinline__ ErfGauss erf_gauss_as(float u) {
+  const float z = fabsf(u) * 0.70710678118654752f;
+  const float t = __builtin_amdgcn_rcpf(fmaf(0.3275911f, z, 1.f));
+  float p = fmaf(1.061405429f, t, -1.453152027f);
+  p = fmaf(p, t, 1.421413741f);
+  p = fmaf(p, t, -0.284496736f);
+  p = fmaf(p, t, 0.254829592f);
+  p *= t;
+  const float g = __builtin_amdgcn_exp2f(-0.72134752044448170f * u * u);  // exp(-u^2/2) = 2^(-u^2 log2(e)/2)
+  const float e = fmaf(-p, g, 1.f);
+  return {copysignf(e, u), g};
+}
+__device__ __forceinline__ float gelu_fast(float u) {
+  return 0.5f * u * (1.f + erf_gauss_as(u).erf_z);
+}
+__device__ __forceinline__ float gelu_grad_fast(float u) {
+  const ErfGauss eg = erf_gauss_as(u);
+  return fmaf(u * 0.39894228040143268f, eg.gauss, 0.5f * (1.f + eg.erf_z));
+}
+
 // ---------------------------------------------------------------- MFMA
 // D[32x32] += A[32x16] * B[16x32]; lane l supplies A[l%32][8*(l/32)+v] and
 // B[8*(l/32)+v][l%32]; D lane l holds D[8*(r/4)+4*(l/32)+r%4][l%32].

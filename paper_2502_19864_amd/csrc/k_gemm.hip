@@ -2,9 +2,13 @@
 // copy of W) and the dX-only backward dY @ W^T of frozen weights, with the
 // elementwise work of the block fused into the epilogue.
 //
-// bf16: MFMA 32x32x16 tiles staged through LDS (double-buffered).  The MFMA
-// computes C^T blocks so that each lane ends up owning four consecutive
-// output columns of one row, which the epilogue stores as one 8-byte write.
+// bf16: MFMA 32x32x16 with large per-wave tiles, operands moved global -> LDS
+// by DMA in a multi-stage pipeline, fragment reads overlapped with the MFMAs,
+// and an epilogue that stages the output tile through LDS so that every
+// global access is a whole-row 16-B vector (gemm_bf16_pipe_body).  A
+// register-staged variant (gemm_bf16_body) covers the shapes the pipelined
+// kernel does not take.  The MFMA computes C^T blocks so that each lane owns
+// four consecutive output columns of one row.
 // f32: a plain FMA tile kernel (used by the small fp32 stage only).
 #include <type_traits>
 
@@ -27,7 +31,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n, float
     if constexpr (E == Epi::Gelu) {
       if (a.out2) St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + n, v);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = gelu_f(v[i]);
+      for (int i = 0; i < 4; ++i) v[i] = std::is_same_v<T, float> ? gelu_f(v[i]) : gelu_fast(v[i]);
     }
     St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, v);
   } else if constexpr (E == Epi::Resid) {
@@ -40,7 +44,7 @@ __device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n, float
     float x[4];
     St<T>::ld4(static_cast<const T*>(a.aux), r * a.ld_aux + n, x);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] *= gelu_grad_f(x[i]);
+    for (int i = 0; i < 4; ++i) v[i] *= std::is_same_v<T, float> ? gelu_grad_f(x[i]) : gelu_grad_fast(x[i]);
     St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, v);
   } else if constexpr (E == Epi::DSwiGlu) {
     float g[4], u[4], dg[4], du[4];
@@ -69,6 +73,73 @@ __device__ __forceinline__ void epilogue_swiglu4(const GemmArgs& a, int m, int f
   if (a.out2) {
     St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + f, g);
     St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + a.half + f, u);
+  }
+}
+
+// eight consecutive bf16 (16-B aligned) <-> float
+__device__ __forceinline__ void ld8(const bf16* p, float v[8]) {
+  unpack_frag(*reinterpret_cast<const bf16x8*>(p), v);
+}
+__device__ __forceinline__ void st8(bf16* p, const float v[8]) {
+  *reinterpret_cast<bf16x8*>(p) = pack_frag(v);
+}
+
+// bf16 epilogue on eight consecutive output columns n..n+7 of row m
+template <Epi E>
+__device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float v[8]) {
+  const long r = m;
+  bf16* out = static_cast<bf16*>(a.out);
+  if constexpr (E == Epi::Store || E == Epi::Gelu) {
+    if (a.bias) {
+      float b[8];
+      ld8(static_cast<const bf16*>(a.bias) + n, b);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] += b[i];
+    }
+    if constexpr (E == Epi::Gelu) {
+      if (a.out2) st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + n, v);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) v[i] = gelu_fast(v[i]);
+    }
+    st8(out + r * a.ldo + n, v);
+  } else if constexpr (E == Epi::Resid) {
+    float x[8];
+    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, x);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] += x[i];
+    st8(out + r * a.ldo + n, v);
+  } else if constexpr (E == Epi::DGelu) {
+    float x[8];
+    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, x);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) v[i] *= gelu_grad_fast(x[i]);
+    st8(out + r * a.ldo + n, v);
+  } else if constexpr (E == Epi::DSwiGlu) {
+    float g[8], u[8], dg[8], du[8];
+    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, g);
+    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + a.half + n, u);
+#pragma unroll
+    for (int i = 0; i < 8; ++i) {
+      const float sg = sigmoid_f(g[i]);
+      du[i] = v[i] * g[i] * sg;
+      dg[i] = v[i] * u[i] * (sg + g[i] * sg * (1.f - sg));
+    }
+    st8(out + r * a.ldo + n, dg);
+    st8(out + r * a.ldo + a.half + n, du);
+  }
+}
+
+// SwiGLU on eight gate/up pairs: feature columns f..f+7
+__device__ __forceinline__ void epilogue_swiglu8(const GemmArgs& a, int m, int f, const float g[8],
+                                                 const float u[8]) {
+  const long r = m;
+  float o[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) o[i] = g[i] * sigmoid_f(g[i]) * u[i];
+  st8(static_cast<bf16*>(a.out) + r * a.ldo + f, o);
+  if (a.out2) {
+    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + f, g);
+    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + a.half + f, u);
   }
 }
 
@@ -222,9 +293,19 @@ __device__ __forceinline__ void tile_coords(int M, int N, int& m0, int& n0) {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-// 16 B per lane, global -> LDS; lane i of the wave lands at lds + 16 i
-__device__ __forceinline__ void dma16(const void* g, void* lds) {
-  __builtin_amdgcn_global_load_lds(g, (lds_ptr_t)lds, 16, 0, 0);
+// Global -> LDS DMA, 16 B per lane (lane i lands at the LDS address + 16 i),
+// issued from inline assembly: scalar base + 32-bit per-lane byte
+// offset, LDS destination (wave-uniform byte address) in M0.  The compiler's
+// wait-count pass does not see these loads, so it inserts no vmcnt waits of
+// its own before LDS reads; the kernel waits for them explicitly (vmcnt
+// counts them like any vector load).  Kernels using this touch M0 nowhere
+// else.
+__device__ __forceinline__ void dma16_m0(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(gbase)
+               : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_ptr_t)p;
 }
 
 template <int N>
@@ -232,37 +313,50 @@ __device__ __forceinline__ void wait_vm_lgkm() {  // vmcnt <= N and lgkmcnt == 0
   static_assert(N >= 0 && N < 64, "vmcnt range");
   __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | ((N >> 4) << 14));
 }
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] at [15:14]
-  __builtin_amdgcn_s_waitcnt((N & 0xF) | (0x7 << 4) | (0xF << 8) | ((N >> 4) << 14));
+
+// ---------------------------------------------------------------- bf16 MFMA kernel, pipelined fragments
+// Large per-wave tiles (FM x FN blocks of 32x32) so that the LDS bytes read
+// per MFMA stay well under the LDS bandwidth, one workgroup of WM x WN waves
+// per CU, operand tiles global -> LDS by DMA, NS stages of BK columns each.
+// Inside a k-tile the fragments of k-step ks+1 are read while the MFMAs of
+// step ks run.  The wait + barrier for the next k-tile sits inside the last
+// k-step, just before its fragments are read, and the stage of the finished
+// k-tile is refilled right after that barrier; so the MFMA pipe does not
+// drain at k-tile boundaries.
+// LDS rows are BK bf16; with CPR = BK/8 16-B chunks per row, chunk c of row r
+// sits at position c ^ swz(r), swz(r) = (r / (16 / CPR)) % CPR, so any 16
+// consecutive rows read at one chunk hit all 64 banks once.
+// Requires K % BK == 0; rows past M or N are clamped (their results are never
+// stored).
+// rows of fp32 output per epilogue pass: BM halved until the pass fits
+constexpr int epi_rows(int bm, int row_bytes, int lds_bytes) {
+  int r = bm;
+  while (r > 32 && r * row_bytes > lds_bytes) r /= 2;
+  return r;
 }
 
-template <int BM, int BN, int WM, int WN, int NS, Epi E, int GROUP = 4>
-__device__ __forceinline__ void gemm_bf16_dma_body(const GemmArgs& a) {
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int ROWB = 128;
+template <int BM, int BN, int WM, int WN, int BK, int NS, Epi E, int GROUP = 4>
+__device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
+  constexpr int NW = WM * WN;
+  constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
+  constexpr int ROWB = BK * 2, CPR = BK / 8, RPI = 64 / CPR, SWD = 16 / CPR;
+  constexpr int LA = BM / (RPI * NW), LB = BN / (RPI * NW), LPT = LA + LB;
+  constexpr int KS = BK / 16;
   constexpr int STAGE = (BM + BN) * ROWB;
-  constexpr int LA = BM / 32, LB = BN / 32, LPT = LA + LB;  // load instructions per wave per k-tile
-  static_assert(WM * WN == 4, "four waves");
-  static_assert(LPT * (NS - 2) < 64, "vmcnt range");
+  static_assert(LA * RPI * NW == BM && LB * RPI * NW == BN, "DMA rows must tile the block");
+  static_assert(FM * 32 * WM == BM && FN * 32 * WN == BN, "wave tiles of 32x32 blocks");
+  static_assert(KS % 2 == 0, "even number of k-steps per tile");
+  static_assert(NS >= 2 && NS <= 4 && LPT * (NS - 1) < 64, "stages / vmcnt range");
   static_assert(E != Epi::SwiGlu || FN % 2 == 0, "SwiGlu needs gate/up block pairs");
-  // one LDS array per stage, so that reads of one stage provably do not alias
-  // the DMA writes in flight to the others (no compiler-inserted vmcnt waits)
-  __shared__ __attribute__((aligned(1024))) char st0[STAGE];
-  __shared__ __attribute__((aligned(1024))) char st1[STAGE];
-  __shared__ __attribute__((aligned(1024))) char st2[NS > 2 ? STAGE : 16];
-  __shared__ __attribute__((aligned(1024))) char st3[NS > 3 ? STAGE : 16];
-  static_assert(NS >= 2 && NS <= 4, "2 to 4 stages");
-  auto stage_base = [&](auto S) -> char* {
-    constexpr int s_ = decltype(S)::value;
-    if constexpr (s_ == 0) return st0;
-    else if constexpr (s_ == 1) return st1;
-    else if constexpr (s_ == 2) return st2;
-    else return st3;
-  };
+  // output tile staging for the epilogue: fp32 rows of BN + 4 (the 16-B pad
+  // spreads the rows one fragment store touches over all banks), RPP rows
+  // (a multiple of 32) per pass through the stage buffers
+  constexpr int CPF = BN + 4;
+  constexpr int RPP = epi_rows(BM, CPF * 4, NS * STAGE);
+  static_assert(RPP >= 32 && BM % RPP == 0 && RPP * CPF * 4 <= NS * STAGE, "epilogue passes of whole 32-row blocks");
+  // the DMA is invisible to the compiler, so one array serves every stage
+  __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
+  auto stage_base = [&](auto S) -> char* { return smem + decltype(S)::value * STAGE; };
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int wm = wave / WN, wn = wave % WN;
@@ -272,26 +366,30 @@ __device__ __forceinline__ void gemm_bf16_dma_body(const GemmArgs& a) {
   const bf16* B = static_cast<const bf16*>(a.B);
   const int M = a.M, N = a.N, K = a.K;
 
-  const int lrow = lane >> 3, lpos = lane & 7;
-  const bf16* ga[LA];
-  const bf16* gb[LB];
+  // DMA: instruction i of this wave fills rows (i*NW + wave)*RPI .. +RPI-1;
+  // lane -> row lane / CPR, LDS position lane % CPR.  Byte offsets from the
+  // operand base (the caller keeps operands under 4 GiB).
+  const int lrow = lane / CPR, lpos = lane % CPR;
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  uint32_t oa[LA], ob[LB];
 #pragma unroll
   for (int i = 0; i < LA; ++i) {
-    const int r = i * 32 + wave * 8 + lrow;
-    ga[i] = A + (long)min(m0 + r, M - 1) * a.lda + ((lpos ^ ((r >> 1) & 7)) * 8);
+    const int r = (i * NW + wave) * RPI + lrow;
+    oa[i] = (uint32_t)(((long)min(m0 + r, M - 1) * a.lda + (lpos ^ ((r / SWD) % CPR)) * 8) * 2);
   }
 #pragma unroll
   for (int i = 0; i < LB; ++i) {
-    const int r = i * 32 + wave * 8 + lrow;
-    gb[i] = B + (long)min(n0 + r, N - 1) * a.ldb + ((lpos ^ ((r >> 1) & 7)) * 8);
+    const int r = (i * NW + wave) * RPI + lrow;
+    ob[i] = (uint32_t)(((long)min(n0 + r, N - 1) * a.ldb + (lpos ^ ((r / SWD) % CPR)) * 8) * 2);
   }
   auto issue = [&](int kt, char* sb) {
+    const char* gA = reinterpret_cast<const char*>(A) + (long)kt * BK * 2;
+    const char* gB = reinterpret_cast<const char*>(B) + (long)kt * BK * 2;
+    const uint32_t l0 = lds_addr(sb);
 #pragma unroll
-    for (int i = 0; i < LA; ++i)
-      dma16(ga[i] + kt * 64, sb + (i * 32 + wave * 8) * ROWB);
+    for (int i = 0; i < LA; ++i) dma16_m0(gA, oa[i], l0 + (i * NW + wave_u) * RPI * ROWB);
 #pragma unroll
-    for (int i = 0; i < LB; ++i)
-      dma16(gb[i] + kt * 64, sb + (BM + i * 32 + wave * 8) * ROWB);
+    for (int i = 0; i < LB; ++i) dma16_m0(gB, ob[i], l0 + (BM + (i * NW + wave_u) * RPI) * ROWB);
   };
 
   f32x16 acc[FM][FN];
@@ -302,50 +400,63 @@ __device__ __forceinline__ void gemm_bf16_dma_body(const GemmArgs& a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
 
-  const int nk = K / 64;
-  const int l32 = lane & 31, half = lane >> 5, sw = (lane >> 1) & 7;
-  issue(0, st0);
-  if constexpr (NS > 2) if (1 < nk) issue(1, st1);
-  if constexpr (NS > 3) if (2 < nk) issue(2, st2);
-  // One k-tile in stage S: wait for this wave's loads of it, barrier (every
-  // wave's loads landed; every wave finished reading the previous stage, whose
-  // fragments fed its previous MFMAs), refill that previous stage with tile
-  // kt + NS - 1, read fragments, multiply.  Two workgroups fit per CU, so one
-  // wave's fragment reads overlap another's MFMAs.
-  auto step = [&](auto S, int kt) {
-    constexpr int s_ = decltype(S)::value;
-    const int later = min(NS - 2, nk - 1 - kt);  // tiles after kt already issued
-    if constexpr (NS >= 4) {
-      if (later >= 2) wait_vmcnt<2 * LPT>();
-      else if (later == 1) wait_vmcnt<LPT>();
-      else wait_vmcnt<0>();
-    } else if constexpr (NS == 3) {
-      if (later >= 1) wait_vmcnt<LPT>();
-      else wait_vmcnt<0>();
-    } else {
-      wait_vmcnt<0>();
-    }
+  const int nk = K / BK;
+  const int l32 = lane & 31, half = lane >> 5, sw = (l32 / SWD) % CPR;
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto read_frags = [&](const char* base, int ks, int slot) {
+    const int off = 16 * ((2 * ks + half) ^ sw);
+    const char* sa = base + (wm * TM + l32) * ROWB + off;
+    const char* sb = base + (BM + wn * TN + l32) * ROWB + off;
+#pragma unroll
+    for (int i = 0; i < FM; ++i) fa[slot][i] = *reinterpret_cast<const bf16x8*>(sa + i * 32 * ROWB);
+#pragma unroll
+    for (int j = 0; j < FN; ++j) fb[slot][j] = *reinterpret_cast<const bf16x8*>(sb + j * 32 * ROWB);
+  };
+  auto mfmas = [&](int slot) {
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(fb[slot][j], fa[slot][i], acc[i][j]);
+  };
+  // vmcnt <= n * LPT and lgkmcnt == 0, for a run-time n in [0, NS-1]
+  auto wait_tiles = [&](int n) {
+    if constexpr (NS >= 4) { if (n >= 3) { wait_vm_lgkm<3 * LPT>(); return; } }
+    if constexpr (NS >= 3) { if (n >= 2) { wait_vm_lgkm<2 * LPT>(); return; } }
+    if (n >= 1) { wait_vm_lgkm<LPT>(); return; }
+    wait_vm_lgkm<0>();
+  };
+  auto barrier = [&] {
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
-    if (kt + NS - 1 < nk) issue(kt + NS - 1, stage_base(std::integral_constant<int, (s_ + NS - 1) % NS>{}));
-    const char* sa = stage_base(S) + (wm * TM + l32) * ROWB;
-    const char* sbb = stage_base(S) + (BM + wn * TN + l32) * ROWB;
-    bf16x8 fa[4][FM], fb[4][FN];
+  };
+
+  // prologue: tiles 0..NS-1 in flight, tile 0 landed, its first fragments read
+  issue(0, smem);
+  if (1 < nk) issue(1, smem + STAGE);
+  if constexpr (NS > 2) if (2 < nk) issue(2, smem + 2 * STAGE);
+  if constexpr (NS > 3) if (3 < nk) issue(3, smem + 3 * STAGE);
+  wait_tiles(min(NS, nk) - 1);
+  barrier();
+  read_frags(smem, 0, 0);
+
+  auto step = [&](auto S, int kt) {
+    constexpr int s_ = decltype(S)::value;
+    constexpr int sn = (s_ + 1) % NS;
+    const char* base = stage_base(S);
 #pragma unroll
-    for (int ks = 0; ks < 4; ++ks) {
-      const int off = 16 * ((2 * ks + half) ^ sw);
-#pragma unroll
-      for (int i = 0; i < FM; ++i) fa[ks][i] = *reinterpret_cast<const bf16x8*>(sa + i * 32 * ROWB + off);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) fb[ks][j] = *reinterpret_cast<const bf16x8*>(sbb + j * 32 * ROWB + off);
+    for (int ks = 0; ks < KS; ++ks) {
+      if (ks + 1 < KS) {
+        read_frags(base, ks + 1, (ks + 1) & 1);
+      } else if (kt + 1 < nk) {
+        // tile kt+1: tiles issued after it are kt+2 .. min(kt+NS-1, nk-1)
+        wait_tiles(min(NS - 2, nk - 2 - kt));
+        barrier();
+        if (kt + NS < nk) issue(kt + NS, stage_base(S));
+        read_frags(stage_base(std::integral_constant<int, sn>{}), 0, 0);
+      }
+      mfmas(ks & 1);
     }
-#pragma unroll
-    for (int ks = 0; ks < 4; ++ks)
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(fb[ks][j], fa[ks][i], acc[i][j]);
   };
   for (int kt = 0; kt < nk; kt += NS) {
     step(std::integral_constant<int, 0>{}, kt);
@@ -354,37 +465,65 @@ __device__ __forceinline__ void gemm_bf16_dma_body(const GemmArgs& a) {
     if constexpr (NS > 3) if (kt + 3 < nk) step(std::integral_constant<int, 3>{}, kt + 3);
   }
 
+  // epilogue: the fp32 tile goes through LDS (row-major, pitch CPF, RPP rows
+  // per pass) so that global traffic is whole-row 16-B vectors; the fused
+  // elementwise work runs on eight-column chunks, on the fp32 sums, with one
+  // rounding to bf16 at the store
+  wait_vm_lgkm<0>();
+  barrier();  // every wave is done reading operand tiles
+  float* cf = reinterpret_cast<float*>(smem);
+  auto ld_tile8 = [&](int row, int col, float v[8]) {
+    const float4 lo = *reinterpret_cast<const float4*>(cf + row * CPF + col);
+    const float4 hi = *reinterpret_cast<const float4*>(cf + row * CPF + col + 4);
+    v[0] = lo.x; v[1] = lo.y; v[2] = lo.z; v[3] = lo.w;
+    v[4] = hi.x; v[5] = hi.y; v[6] = hi.z; v[7] = hi.w;
+  };
 #pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * TM + i * 32 + l32;
-    if (m >= M) continue;
-    if constexpr (E == Epi::SwiGlu) {
+  for (int p = 0; p < BM / RPP; ++p) {
 #pragma unroll
-      for (int j = 0; j < FN; j += 2) {
-        const int ng = n0 + wn * TN + j * 32;
-        if (ng >= N) continue;
-        const int fbase = (ng / 64) * 32;
+    for (int i = 0; i < FM; ++i) {
+      if ((wm * TM + i * 32) / RPP != p) continue;  // wave-uniform
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          float gv[4], uv[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) { gv[q] = acc[i][j][4 * g + q]; uv[q] = acc[i][j + 1][4 * g + q]; }
-          epilogue_swiglu4<bf16>(a, m, fbase + 8 * g + 4 * half, gv, uv);
+          const int row = wm * TM + i * 32 + l32 - p * RPP, col = wn * TN + j * 32 + 8 * g + 4 * half;
+          *reinterpret_cast<float4*>(cf + row * CPF + col) =
+              make_float4(acc[i][j][4 * g], acc[i][j][4 * g + 1], acc[i][j][4 * g + 2], acc[i][j][4 * g + 3]);
         }
+    }
+    wait_vm_lgkm<0>();
+    barrier();
+    if constexpr (E == Epi::SwiGlu) {
+      // packed columns [64p, 64p+32) are gates, [64p+32, 64p+64) the matching ups
+      constexpr int CPRW = BN / 16, NCH = RPP * CPRW;
+      static_assert(NCH % 256 == 0, "whole passes");
+#pragma unroll 2
+      for (int idx = tid; idx < NCH; idx += 256) {
+        const int row = idx / CPRW, q = idx % CPRW, c = (q / 4) * 64 + (q % 4) * 8;
+        const int m = m0 + p * RPP + row;
+        if (m >= M || n0 + c >= N) continue;
+        float gv[8], uv[8];
+        ld_tile8(row, c, gv);
+        ld_tile8(row, c + 32, uv);
+        epilogue_swiglu8(a, m, (n0 + c) / 64 * 32 + (c % 64), gv, uv);
       }
     } else {
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = n0 + wn * TN + j * 32 + 8 * g + 4 * half;
-          if (n >= N) continue;
-          float v[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
-          epilogue4<E, bf16>(a, m, n, v);
-        }
+      constexpr int CPRW = BN / 8, NCH = RPP * CPRW;
+      static_assert(NCH % 256 == 0, "whole passes");
+#pragma unroll 2
+      for (int idx = tid; idx < NCH; idx += 256) {
+        const int row = idx / CPRW, c = (idx % CPRW) * 8;
+        const int m = m0 + p * RPP + row, n = n0 + c;
+        if (m >= M || n >= N) continue;
+        float v[8];
+        ld_tile8(row, c, v);
+        epilogue8<E>(a, m, n, v);
       }
+    }
+    if (p + 1 < BM / RPP) {
+      wait_vm_lgkm<0>();
+      barrier();  // the next pass overwrites the staging rows
     }
   }
 }
@@ -434,8 +573,8 @@ __device__ __forceinline__ void gemm_f32_body(const GemmArgs& a) {
     gemm_bf16_body<BM, BN, WM, WN, E>(a);                                            \
   }                                                                                  \
   template <int BM, int BN, int WM, int WN, int NS, Epi E>                           \
-  __global__ __launch_bounds__(256) void NAME##_dma(GemmArgs a) {                    \
-    gemm_bf16_dma_body<BM, BN, WM, WN, NS, E, 4>(a);                                 \
+  __global__ __launch_bounds__(256) void NAME##_pipe(GemmArgs a) {                   \
+    gemm_bf16_pipe_body<BM, BN, WM, WN, 64, NS, E, 4>(a);                            \
   }                                                                                  \
   template <Epi E>                                                                   \
   __global__ __launch_bounds__(256) void NAME##_f32(GemmArgs a) {                    \
@@ -468,10 +607,13 @@ static constexpr bool role_has(Role r, Epi e) {
   }
 }
 
-// tile shape: 128x128 with two stages when that gives at least three
-// workgroups per CU (the 2 x 256-CU occupancy is then full twice over), else
-// 64x128 with three stages (measured on the BERT-base stage shapes)
-enum Cfg { C_DMA_128x128, C_DMA_64x128, C_REG_128x128, C_REG_64x128 };
+// Tile shapes of the pipelined kernel (BK = 64), chosen per GEMM shape by
+// measurement on the BERT-base stage: 128x192 (2x2 waves of 64x96) for wide
+// outputs with short K, 128x96 (4x1 waves of 32x96, three stages) for
+// 768-wide outputs, 128x128 (2x2 waves of 64x64) otherwise and for the
+// SwiGLU epilogue, which needs gate/up block pairs in one wave.  The register
+// staged kernel covers K % 64 != 0 and unaligned epilogue operands.
+enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_REG_128x128, C_REG_64x128 };
 
 template <Role R, Epi E>
 static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t s) {
@@ -496,15 +638,22 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
         return hipGetLastError();
       }
     }
+#define RG_TILES(BM, BN) dim3(((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM))
 #define RG_LAUNCH(NAME)                                                                                  \
   switch (cfg) {                                                                                         \
-    case C_DMA_128x128:                                                                                  \
-      hipLaunchKernelGGL((NAME##_dma<128, 128, 2, 2, 2, E>),                                             \
-                         dim3(((a.N + 127) / 128) * ((a.M + 127) / 128)), block, 0, s, a);               \
+    case C_P128x192:                                                                                     \
+      if constexpr (E != Epi::SwiGlu)                                                                    \
+        hipLaunchKernelGGL((NAME##_pipe<128, 192, 2, 2, 2, E>), RG_TILES(128, 192), block, 0, s, a);     \
       break;                                                                                             \
-    case C_DMA_64x128:                                                                                   \
-      hipLaunchKernelGGL((NAME##_dma<64, 128, 2, 2, 3, E>),                                              \
-                         dim3(((a.N + 127) / 128) * ((a.M + 63) / 64)), block, 0, s, a);                 \
+    case C_P128x96:                                                                                      \
+      if constexpr (E != Epi::SwiGlu)                                                                    \
+        hipLaunchKernelGGL((NAME##_pipe<128, 96, 4, 1, 3, E>), RG_TILES(128, 96), block, 0, s, a);       \
+      break;                                                                                             \
+    case C_P128x128_2:                                                                                   \
+      hipLaunchKernelGGL((NAME##_pipe<128, 128, 2, 2, 2, E>), RG_TILES(128, 128), block, 0, s, a);       \
+      break;                                                                                             \
+    case C_P128x128_3:                                                                                   \
+      hipLaunchKernelGGL((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
       break;                                                                                             \
     case C_REG_128x128:                                                                                  \
       hipLaunchKernelGGL((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
@@ -527,6 +676,7 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       default: return hipErrorInvalidValue;
     }
 #undef RG_LAUNCH
+#undef RG_TILES
 #undef RG_NAME
     return hipGetLastError();
   }
@@ -562,10 +712,23 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     if (a.K % 8 || a.lda % 8 || a.ldb % 8 || !al16(a.A) || !al16(a.B) || !al8(a.out))
       return hipErrorInvalidValue;
     if (epi == Epi::SwiGlu && (a.N % 64 || a.half * 2 != a.N)) return hipErrorInvalidValue;
-    const long tiles128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-    const bool big = tiles128 >= 768;
-    if (a.K % 64 == 0) cfg = big ? C_DMA_128x128 : C_DMA_64x128;
-    else cfg = tiles128 >= 512 ? C_REG_128x128 : C_REG_64x128;
+    // pipelined kernel: K in 64-wide tiles, 16-B epilogue vectors, operands
+    // addressed with 32-bit byte offsets
+    const bool al_epi = a.N % 8 == 0 && a.ldo % 8 == 0 && al16(a.out) && (!a.bias || al16(a.bias)) &&
+                        (!a.aux || (al16(a.aux) && a.ld_aux % 8 == 0)) &&
+                        (!a.out2 || (al16(a.out2) && a.ldo2 % 8 == 0)) && a.half % 8 == 0;
+    const bool small_off = ((double)(a.M - 1) * a.lda + a.K) * 2 < 4294967296.0 &&
+                           ((double)(a.N - 1) * a.ldb + a.K) * 2 < 4294967296.0;
+    const long t192 = (long)((a.M + 127) / 128) * ((a.N + 191) / 192);
+    if (a.K % 64 == 0 && al_epi && small_off) {
+      if (epi == Epi::SwiGlu || epi == Epi::DSwiGlu) cfg = a.K <= 1024 ? C_P128x128_2 : C_P128x128_3;
+      else if (a.N % 192 == 0 && a.K <= 1024 && t192 >= 256) cfg = C_P128x192;
+      else if (a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
+      else cfg = a.K <= 1024 ? C_P128x128_2 : C_P128x128_3;
+    } else {
+      const long tiles128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
+      cfg = tiles128 >= 512 ? C_REG_128x128 : C_REG_64x128;
+    }
   } else if (dtype == DT_F32) {
     if (!al16(a.out)) return hipErrorInvalidValue;
   } else {
