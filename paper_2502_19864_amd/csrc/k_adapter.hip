@@ -202,6 +202,167 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   }
 }
 
+// Same computation for d <= 1024, laid out so that nothing waits twice on
+// memory and every global row access is contiguous: all global loads (the z
+// tile, the weight fragments of both projections, the residual) are issued
+// before the first barrier; the up projection's fp32 result is staged in LDS;
+// the add + norm phase then runs one wave per token (NW == TOK), so the row
+// statistics are wave reductions and each lane handles features
+// 4*lane + 256*j, which makes every load and store of that phase one
+// contiguous 512-B run per instruction.
+template <int FB>
+__global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
+  constexpr int NW = 16, KS = 4;
+  constexpr int D = 256 * FB, DP = D + 8, VP = D + 4;
+  constexpr int SLICE = D / KS, NSTEP = SLICE / 32;
+  static_assert(NW == TOK, "one wave per token in the norm phase");
+  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  bf16* sZ = reinterpret_cast<bf16*>(smem);                // [TOK][DP]
+  bf16* sG = sZ + TOK * DP;                                // [TOK][GP]
+  float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][TOK][MB]
+  float* sV = sUp + KS * TOK * MB;                         // [TOK][VP]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int T = a.T, t0 = blockIdx.x * TOK;
+  const bf16* z = static_cast<const bf16*>(a.z);
+
+  // ---- every global load up front
+  constexpr int CPR = D / 8, NCH = TOK * CPR, PER = (NCH + 1023) / 1024;
+  uint4 zv[PER];
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int c = threadIdx.x + i * 1024, r = c / CPR, k = (c % CPR) * 8;
+    zv[i] = (c < NCH && t0 + r < T) ? *reinterpret_cast<const uint4*>(z + (long)(t0 + r) * D + k)
+                                    : make_uint4(0, 0, 0, 0);
+  }
+  const int ug = wave % 4, ks = wave / 4;
+  bf16x8 wd[NSTEP];
+  {
+    const bf16* p = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
+#pragma unroll
+    for (int j = 0; j < NSTEP; ++j) wd[j] = ld_frag(p + j * 32);
+  }
+  const int f0 = wave * 16 * FB;
+  bf16x8 w0[FB], w1[FB];
+  {
+    const bf16* p = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      w0[b] = ld_frag(p + (long)b * 16 * MB);
+      w1[b] = ld_frag(p + (long)b * 16 * MB + 32);
+    }
+  }
+  const int tw = t0 + wave;  // this wave's token in the norm phase
+  const bool twv = tw < T;
+  const long wrow = (long)(twv ? tw : 0) * D;
+  uint2 rr[FB];
+#pragma unroll
+  for (int j = 0; j < FB; ++j)
+    rr[j] = twv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + 4 * lane + 256 * j)
+                : make_uint2(0, 0);
+#pragma unroll
+  for (int i = 0; i < PER; ++i) {
+    const int c = threadIdx.x + i * 1024, r = c / CPR, k = (c % CPR) * 8;
+    if (c < NCH) *reinterpret_cast<uint4*>(sZ + r * DP + k) = zv[i];
+  }
+  __syncthreads();
+
+  // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:], k split over KS waves
+  {
+    const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
+    f32x4 u = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int j = 0; j < NSTEP; ++j) u = mfma16(wd[j], ld_frag(zr + j * 32), u);
+#pragma unroll
+    for (int r = 0; r < 4; ++r) sUp[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = u[r];
+    __syncthreads();
+    if (ks == 0) {
+      float uv[4], gv[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        float s = 0.f;
+#pragma unroll
+        for (int k2 = 0; k2 < KS; ++k2) s += sUp[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
+        uv[r] = s;
+        gv[r] = gelu_fast(s);
+      }
+      if (a.u && t0 + l16 < T) St<bf16>::st4(static_cast<bf16*>(a.u), (long)(t0 + l16) * MB + ug * 16 + 4 * grp, uv);
+      St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
+    }
+  }
+  __syncthreads();
+
+  // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  -> sV (fp32)
+  {
+    const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mfma16(w0[b], g0, acc);
+      acc = mfma16(w1[b], g1, acc);
+      *reinterpret_cast<float4*>(sV + l16 * VP + f0 + b * 16 + 4 * grp) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+  }
+  __syncthreads();
+
+  // ---- add + norm, wave = token
+  if (!twv) return;
+  float v[FB][4];
+#pragma unroll
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    const float4 up = *reinterpret_cast<const float4*>(sV + wave * VP + f);
+    float zz[4];
+    St<bf16>::ld4(sZ, wave * DP + f, zz);
+    const float r4[4] = {__uint_as_float(rr[j].x << 16), __uint_as_float(rr[j].x & 0xffff0000u),
+                         __uint_as_float(rr[j].y << 16), __uint_as_float(rr[j].y & 0xffff0000u)};
+    v[j][0] = up.x + zz[0] + r4[0];
+    v[j][1] = up.y + zz[1] + r4[1];
+    v[j][2] = up.z + zz[2] + r4[2];
+    v[j][3] = up.w + zz[3] + r4[3];
+  }
+  if (a.norm == Norm::None) {
+#pragma unroll
+    for (int j = 0; j < FB; ++j) St<bf16>::st4(static_cast<bf16*>(a.out), wrow + 4 * lane + 256 * j, v[j]);
+    return;
+  }
+  constexpr float inv_d = 1.f / (float)D;
+  float mean = 0.f;
+  if (a.norm == Norm::LN) {
+    float s = 0.f;
+#pragma unroll
+    for (int j = 0; j < FB; ++j) s += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
+    mean = wave_sum(s) * inv_d;
+  } else {
+#pragma unroll
+    for (int j = 0; j < FB; ++j)  // RMS: the residual stream h itself is an output
+      St<bf16>::st4(static_cast<bf16*>(a.out), wrow + 4 * lane + 256 * j, v[j]);
+  }
+  float s2 = 0.f;
+#pragma unroll
+  for (int j = 0; j < FB; ++j)
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const float c = v[j][q] - mean;
+      s2 += c * c;
+    }
+  const float rstd = rsqrtf(wave_sum(s2) * inv_d + a.eps);
+  if (a.rstd && lane == 0) a.rstd[tw] = rstd;
+  bf16* out = static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm);
+#pragma unroll
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    float xh[4], gm[4], bt[4] = {0.f, 0.f, 0.f, 0.f}, o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) xh[q] = (v[j][q] - mean) * rstd;
+    St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
+    if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
+#pragma unroll
+    for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
+    St<bf16>::st4(out, wrow + f, o);
+    if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), wrow + f, xh);
+  }
+}
+
 // ================================================================ bf16 backward
 template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
@@ -584,6 +745,22 @@ static bool bf16_shape(int d, int& nw, int& fb) {
   return false;
 }
 
+template <int FB>
+static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
+  constexpr int D = 256 * FB;
+  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)4 * TOK * MB * 4 +
+                    (size_t)TOK * (D + 4) * 4;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_fwd_rows<FB>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)sh);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  hipLaunchKernelGGL((adapter_fwd_rows<FB>), dim3((a.T + TOK - 1) / TOK), dim3(1024), sh, s, a);
+  return hipGetLastError();
+}
+
 template <int NW, int FB>
 static hipError_t fwd_k(const AdapterFwdArgs& a, hipStream_t s) {
   constexpr int D = 16 * NW * FB;
@@ -627,10 +804,10 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
     if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.z) || !al16(a.wdn_t) || !al16(a.wup_t))
       return hipErrorInvalidValue;
     switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
-      case 1: return fwd_k<16, 1>(a, s);
-      case 2: return fwd_k<16, 2>(a, s);
-      case 3: return fwd_k<16, 3>(a, s);
-      case 4: return fwd_k<16, 4>(a, s);
+      case 1: return fwd_rows_k<1>(a, s);
+      case 2: return fwd_rows_k<2>(a, s);
+      case 3: return fwd_rows_k<3>(a, s);
+      case 4: return fwd_rows_k<4>(a, s);
       case 8: return fwd_k<16, 8>(a, s);
       case 12: return fwd_k<16, 12>(a, s);
       case 16: return fwd_k<16, 16>(a, s);

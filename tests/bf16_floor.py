@@ -1,9 +1,11 @@
-"""bf16 noise floor of the pre-RMS (LLaMA-shaped) stage, by emulation.
+"""bf16 noise floor of the stage, by emulation.
 
-Test infrastructure.  The float64 oracle's pre-RMS block forward, re-run with
-every intermediate that the bf16 HIP path stores in bf16 rounded to bf16
-(round to nearest even) and everything else in float64, then the oracle's
-exact backward from those caches.  Its deviation from the plain oracle is a
+Test infrastructure.  The float64 oracle's block forward (pre-RMS LLaMA-shaped
+or post-LN BERT-shaped), re-run with every intermediate that the bf16 HIP path
+stores in bf16 rounded to bf16 (round to nearest even) and everything else in
+float64, then the oracle's exact backward from those caches (and, for a loss
+computed on the stage output, the loss gradient of the emulated output,
+rounded to bf16 as the path stores it).  Its deviation from the plain oracle is a
 lower bound on the error ANY implementation with bf16 intermediates incurs on
 this workload (it ignores the backward's own roundings), and so a floor for
 the parity tolerance of that workload.  Uses no value from the HIP path.
@@ -50,6 +52,81 @@ def llama_block_fwd_bf16(desc, w, ad, x, B, S):
     cache = dict(xhat1=xhat1, rstd1=rstd1, q=q, k=k, v=v, p=p, attn=attn, u1=u1, xhat2=xhat2,
                  rstd2=rstd2, gate=gate, up=up, f=f, u2=u2, cos=cos, sin=sin)
     return y, cache
+
+
+def bert_block_fwd_bf16(desc, w, ad, x, B, S):
+    """oracle.bert_block_fwd with the bf16 path's storage roundings: the QKV
+    projection, the unnormalised attention probabilities fed to the PV
+    product, the attention output and out-projection, the adapters' stashed
+    down-projections and their GELU (fed to the up-projection), the LayerNorm
+    outputs and their normalised inputs, the FFN pre-activation stash and its
+    GELU, the FFN output."""
+    H, eps = desc["n_heads"], desc["norm_eps"]
+    d = x.shape[1]
+    qkv = _rb(x @ w["w_qkv"] + w["b_qkv"])
+    q = O.split_heads(qkv[:, :d], B, S, H)
+    k = O.split_heads(qkv[:, d:2 * d], B, S, H)
+    v = O.split_heads(qkv[:, 2 * d:], B, S, H)
+    o_h, p = O.attention_fwd(q, k, v, causal=False)
+    # the path feeds exp(s - max) to the PV product in bf16 and divides by the
+    # float row sum afterwards
+    s_ = q @ np.swapaxes(k, -1, -2) / np.sqrt(q.shape[-1])
+    e_ = np.exp(s_ - s_.max(axis=-1, keepdims=True))
+    o_h = (_rb(e_) @ v) / e_.sum(axis=-1, keepdims=True)
+    attn = _rb(_rb(O.merge_heads(o_h)) @ w["w_o"] + w["b_o"])
+    U1 = attn @ ad[0]["w_down"]
+    a = attn + _rb(O.gelu(U1)) @ ad[0]["w_up"]
+    h1, xhat1, rstd1 = O.layer_norm(x + a, w["ln1_g"], w["ln1_b"], eps)
+    h1 = _rb(h1)
+    A1 = h1 @ w["w_i"] + w["b_i"]
+    f2 = _rb(_rb(O.gelu(A1)) @ w["w_f"] + w["b_f"])
+    U2 = f2 @ ad[1]["w_down"]
+    fa = f2 + _rb(O.gelu(U2)) @ ad[1]["w_up"]
+    y, xhat2, rstd2 = O.layer_norm(h1 + fa, w["ln2_g"], w["ln2_b"], eps)
+    cache = dict(q=q, k=k, v=v, p=p, attn=attn, u1=_rb(U1), xhat1=_rb(xhat1), rstd1=rstd1, a1=_rb(A1),
+                 f2=f2, u2=_rb(U2), xhat2=_rb(xhat2), rstd2=rstd2)
+    return _rb(y), cache
+
+
+def bert_floor(w, inp, c, ref):
+    """Per-tensor deviation (max |.| / max |ref|) of the bf16-emulated run of
+    a post-LN workload (its own loss included) from the oracle run `ref`
+    (helpers.oracle_run at the same cut-off c): {'y': e, 'g_wh': e (CE loss),
+    (l, a, name): e}."""
+    desc = oracle_desc(w)
+    W, A = to64(inp, w)
+    x = np.asarray(inp["x"], np.float64)
+    Bb, S, d = x.shape
+    h = x.reshape(Bb * S, d)
+    caches = []
+    for l in range(w.n_blocks):
+        h, cache = bert_block_fwd_bf16(desc, W[l], A[l], h, Bb, S)
+        caches.append(cache)
+    y = h.reshape(Bb, S, d)
+    out = {"y": rel_err(y, ref["y"])}
+    if w.loss == "cls_ce":
+        _, dy, gwh, _ = O.cls_head_ce(y, inp["w_h"].astype(np.float64), inp["b_h"].astype(np.float64),
+                                      inp["labels"])
+        out["g_wh"] = rel_err(gwh, ref["g_wh"])
+        dy = _rb(dy)
+    elif w.loss == "mse":
+        _, dy = O.mse_loss(y, inp["target"].astype(np.float64))
+        dy = _rb(dy)
+    else:
+        dy = np.asarray(inp["dy"], np.float64)
+    _, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
+    for l in range(max(c, 0), w.n_blocks):
+        for a in range(2):
+            for k in ("w_down", "w_up"):
+                out[(l, a, k)] = rel_err(g_emu[l][a][k], ref["grads"][l][a][k])
+    return out
+
+
+def floor_bound(floor, key):
+    """Parity bound of one bf16 output tensor: the stated 2e-2, or twice the
+    emulated storage floor of that tensor where the floor alone is beyond
+    half of it."""
+    return max(2e-2, 2.0 * floor[key])
 
 
 def llama_floor(w, inp, c, dy, batch, seq):

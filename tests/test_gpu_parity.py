@@ -77,6 +77,9 @@ def run_gpu(torch, stage, w, inp, c, dy=None, want_dx=False):
 
 
 def check_grads(gpu, ref, lo, L, tol, tag):
+    """Every adapter gradient against the oracle; `tol` is a bound or a
+    function of the tensor key (l, a, name)."""
+    bound = tol if callable(tol) else (lambda key: tol)
     worst = 0.0
     for l in range(L):
         for a in range(2):
@@ -87,9 +90,20 @@ def check_grads(gpu, ref, lo, L, tol, tag):
                     continue
                 e = rel_err(g, ref["grads"][l][a][k])
                 worst = max(worst, e)
-                assert e <= tol, (tag, l, a, k, e)
+                assert e <= bound((l, a, k)), (tag, l, a, k, e, bound((l, a, k)))
     print(f"[{tag}] worst adapter-gradient error {worst:.3e}", flush=True)
     return worst
+
+
+def floor_bounds(w, inp, c, ref):
+    """Per-tensor bounds of a bf16 post-LN workload: 2e-2, or twice the bf16
+    storage floor of the tensor (tests/bf16_floor.py) where that is larger."""
+    from bf16_floor import bert_floor, floor_bound
+    fl = bert_floor(w, inp, c, ref)
+    over = {k: v for k, v in fl.items() if 2.0 * v > 2e-2}
+    print(f"[{w.name}] bf16 storage floor: max {max(fl.values()):.3e}; bounds above 2e-2: "
+          + ", ".join(f"{k}: {2 * v:.3e}" for k, v in sorted(over.items(), key=str)), flush=True)
+    return lambda key: floor_bound(fl, key)
 
 
 @pytest.mark.parametrize("name", sorted(SMALL))
@@ -140,10 +154,12 @@ def test_bert_base_workload_parity(torch):
     try:
         gpu = run_gpu(torch, st, w, inp, w.lowest_unfrozen)
         ref = oracle_run(w, inp, w.lowest_unfrozen)
-        assert rel_err(gpu["y"], ref["y"]) <= 2e-2
+        bound = floor_bounds(w, inp, w.lowest_unfrozen, ref)
+        print(f"[bert_base] y error {rel_err(gpu['y'], ref['y']):.3e}", flush=True)
+        assert rel_err(gpu["y"], ref["y"]) <= bound("y")
         assert abs(gpu["loss"][0] - ref["loss"]) <= 2e-2 * abs(ref["loss"])
-        assert rel_err(gpu["g_wh"], ref["g_wh"]) <= 2e-2
-        check_grads(gpu, ref, w.lowest_unfrozen, w.n_blocks, 2e-2, "bert_base")
+        assert rel_err(gpu["g_wh"], ref["g_wh"]) <= bound("g_wh")
+        check_grads(gpu, ref, w.lowest_unfrozen, w.n_blocks, bound, "bert_base")
         # adapter update (SGD), then a second forward with the updated adapters
         lr = 0.5
         st.step(w.lowest_unfrozen, lr)
@@ -157,14 +173,14 @@ def test_bert_base_workload_parity(torch):
                     old = inp["adapters"][l][a][k]
                     if l >= w.lowest_unfrozen:
                         # the applied step -lr * g matches the oracle's
-                        assert rel_err(got - old, new_ad[l][a][k] - old) <= 2e-2, (l, a, k)
+                        assert rel_err(got - old, new_ad[l][a][k] - old) <= bound((l, a, k)), (l, a, k)
                     else:
                         assert np.array_equal(got, old), (l, a, k)
                     assert np.all(st.adapters[l][a]["g_" + k[2:]].cpu().numpy() == 0)
         inp2 = dict(inp, adapters=new_ad)
         gpu2 = run_gpu(torch, st, w, inp2, w.n_blocks)  # frozen forward, no backward
         ref2 = oracle_run(w, inp2, w.n_blocks)
-        assert rel_err(gpu2["y"], ref2["y"]) <= 2e-2
+        assert rel_err(gpu2["y"], ref2["y"]) <= bound("y")
     finally:
         st.close()
 
@@ -175,13 +191,16 @@ def test_bert_base_unfreezing_sweep(torch):
     w = WORKLOADS["bert_base_sweep"]
     inp = make_inputs(w)
     ref = oracle_run(w, inp, 0)
+    # the truncated backward's gradients are the full backward's, so one floor
+    # run at c = 0 covers every cut-off
+    bound = floor_bounds(w, inp, 0, ref)
     st = Stage(w, inp)
     try:
         for c in SWEEP:
             print(f"[sweep] c={c}", flush=True)
             gpu = run_gpu(torch, st, w, inp, c)
-            assert rel_err(gpu["y"], ref["y"]) <= 2e-2
-            check_grads(gpu, ref, c, w.n_blocks, 2e-2, f"sweep c={c}")
+            assert rel_err(gpu["y"], ref["y"]) <= bound("y")
+            check_grads(gpu, ref, c, w.n_blocks, bound, f"sweep c={c}")
     finally:
         st.close()
 
@@ -193,8 +212,9 @@ def test_bert_large_share_parity(torch):
     try:
         gpu = run_gpu(torch, st, w, inp, w.lowest_unfrozen)
         ref = oracle_run(w, inp, w.lowest_unfrozen)
-        assert rel_err(gpu["y"], ref["y"]) <= 2e-2
-        check_grads(gpu, ref, w.lowest_unfrozen, w.n_blocks, 2e-2, "bert_large")
+        bound = floor_bounds(w, inp, w.lowest_unfrozen, ref)
+        assert rel_err(gpu["y"], ref["y"]) <= bound("y")
+        check_grads(gpu, ref, w.lowest_unfrozen, w.n_blocks, bound, "bert_large")
     finally:
         st.close()
 
