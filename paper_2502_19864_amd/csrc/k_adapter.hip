@@ -757,7 +757,7 @@ static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr = true;
   }
-  hipLaunchKernelGGL((adapter_fwd_rows<FB>), dim3((a.T + TOK - 1) / TOK), dim3(1024), sh, s, a);
+  RG_LAUNCH((adapter_fwd_rows<FB>), dim3((a.T + TOK - 1) / TOK), dim3(1024), sh, s, a);
   return hipGetLastError();
 }
 
@@ -773,7 +773,7 @@ static hipError_t fwd_k(const AdapterFwdArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr = true;
   }
-  hipLaunchKernelGGL((adapter_fwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
+  RG_LAUNCH((adapter_fwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
   return hipGetLastError();
 }
 template <int NW, int FB>
@@ -788,7 +788,7 @@ static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
     if (e != hipSuccess) return e;
     attr = true;
   }
-  hipLaunchKernelGGL((adapter_bwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
+  RG_LAUNCH((adapter_bwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
   return hipGetLastError();
 }
 
@@ -816,7 +816,7 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
   }
   const size_t sh = (2 * (size_t)a.d + a.m + 8) * sizeof(float);
   if (sh > 64 * 1024) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(adapter_fwd_f32, dim3(a.T), dim3(256), sh, s, a);
+  RG_LAUNCH(adapter_fwd_f32, dim3(a.T), dim3(256), sh, s, a);
   return hipGetLastError();
 }
 
@@ -843,7 +843,7 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
   }
   const size_t sh = ((size_t)a.d + a.m + 8) * sizeof(float);
   if (sh > 64 * 1024) return hipErrorInvalidValue;
-  hipLaunchKernelGGL(adapter_bwd_f32, dim3(a.T), dim3(256), sh, s, a);
+  RG_LAUNCH(adapter_bwd_f32, dim3(a.T), dim3(256), sh, s, a);
   return hipGetLastError();
 }
 
@@ -853,11 +853,11 @@ hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s) {
   if (dtype == DT_BF16) {
     if (a.m != MB || a.d % 64) return hipErrorInvalidValue;
     const dim3 grid(a.d / 64, (a.T + DW_TC - 1) / DW_TC, 2);
-    hipLaunchKernelGGL(adapter_dw_bf16, grid, dim3(256), 0, s, a);
+    RG_LAUNCH(adapter_dw_bf16, grid, dim3(256), 0, s, a);
     return hipGetLastError();
   }
   const long n = 2L * a.m * a.d;
-  hipLaunchKernelGGL(adapter_dw_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  RG_LAUNCH(adapter_dw_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -524,19 +524,19 @@ static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) 
 template <int DH>
 static hipError_t fwd_dh(const AttnArgs& a, hipStream_t s) {
   dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
-  if (a.causal) hipLaunchKernelGGL((attn_fwd_bf16<DH, true>), grid, block, 0, s, a);
-  else hipLaunchKernelGGL((attn_fwd_bf16<DH, false>), grid, block, 0, s, a);
+  if (a.causal) RG_LAUNCH((attn_fwd_bf16<DH, true>), grid, block, 0, s, a);
+  else RG_LAUNCH((attn_fwd_bf16<DH, false>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 template <int DH>
 static hipError_t bwd_dh(const AttnArgs& a, hipStream_t s) {
   dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
   if (a.causal) {
-    hipLaunchKernelGGL((attn_bwd_dq_bf16<DH, true>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<DH, true>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dq_bf16<DH, true>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, true>), grid, block, 0, s, a);
   } else {
-    hipLaunchKernelGGL((attn_bwd_dq_bf16<DH, false>), grid, block, 0, s, a);
-    hipLaunchKernelGGL((attn_bwd_dkdv_bf16<DH, false>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dq_bf16<DH, false>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, false>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }
@@ -558,7 +558,7 @@ hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
   hipError_t e = check(dtype, a, false);
   if (e != hipSuccess) return e;
   if (dtype == DT_BF16) return a.dh == 64 ? fwd_dh<64>(a, s) : fwd_dh<128>(a, s);
-  hipLaunchKernelGGL(attn_fwd_f32, dim3(a.B * a.H), dim3(256), 0, s, a);
+  RG_LAUNCH(attn_fwd_f32, dim3(a.B * a.H), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
@@ -566,7 +566,7 @@ hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
   hipError_t e = check(dtype, a, true);
   if (e != hipSuccess) return e;
   if (dtype == DT_BF16) return a.dh == 64 ? bwd_dh<64>(a, s) : bwd_dh<128>(a, s);
-  hipLaunchKernelGGL(attn_bwd_f32, dim3(a.B * a.H), dim3(256), a.S * sizeof(float), s, a);
+  RG_LAUNCH(attn_bwd_f32, dim3(a.B * a.H), dim3(256), a.S * sizeof(float), s, a);
   return hipGetLastError();
 }
 

@@ -628,7 +628,7 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       else {
         dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
         switch (R) {
-#define RG_F32(ROLE, NAME) case ROLE: hipLaunchKernelGGL((NAME##_f32<E>), grid, block, 0, s, a); break;
+#define RG_F32(ROLE, NAME) case ROLE: RG_LAUNCH((NAME##_f32<E>), grid, block, 0, s, a); break;
           RG_F32(R_QKV_FWD, gemm_qkv_fwd) RG_F32(R_O_FWD, gemm_o_fwd) RG_F32(R_FFN_IN_FWD, gemm_ffn_in_fwd)
           RG_F32(R_FFN_OUT_FWD, gemm_ffn_out_fwd) RG_F32(R_QKV_DX, gemm_qkv_dx) RG_F32(R_O_DX, gemm_o_dx)
           RG_F32(R_FFN_IN_DX, gemm_ffn_in_dx) RG_F32(R_FFN_OUT_DX, gemm_ffn_out_dx)
@@ -639,43 +639,43 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       }
     }
 #define RG_TILES(BM, BN) dim3(((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM))
-#define RG_LAUNCH(NAME)                                                                                  \
+#define RG_LAUNCH_CFG(NAME)                                                                                  \
   switch (cfg) {                                                                                         \
     case C_P128x192:                                                                                     \
       if constexpr (E != Epi::SwiGlu)                                                                    \
-        hipLaunchKernelGGL((NAME##_pipe<128, 192, 2, 2, 2, E>), RG_TILES(128, 192), block, 0, s, a);     \
+        RG_LAUNCH((NAME##_pipe<128, 192, 2, 2, 2, E>), RG_TILES(128, 192), block, 0, s, a);     \
       break;                                                                                             \
     case C_P128x96:                                                                                      \
       if constexpr (E != Epi::SwiGlu)                                                                    \
-        hipLaunchKernelGGL((NAME##_pipe<128, 96, 4, 1, 3, E>), RG_TILES(128, 96), block, 0, s, a);       \
+        RG_LAUNCH((NAME##_pipe<128, 96, 4, 1, 3, E>), RG_TILES(128, 96), block, 0, s, a);       \
       break;                                                                                             \
     case C_P128x128_2:                                                                                   \
-      hipLaunchKernelGGL((NAME##_pipe<128, 128, 2, 2, 2, E>), RG_TILES(128, 128), block, 0, s, a);       \
+      RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 2, E>), RG_TILES(128, 128), block, 0, s, a);       \
       break;                                                                                             \
     case C_P128x128_3:                                                                                   \
-      hipLaunchKernelGGL((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
+      RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
       break;                                                                                             \
     case C_REG_128x128:                                                                                  \
-      hipLaunchKernelGGL((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
+      RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
                          s, a);                                                                          \
       break;                                                                                             \
     case C_REG_64x128:                                                                                   \
-      hipLaunchKernelGGL((NAME<64, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 63) / 64), block, 0,   \
+      RG_LAUNCH((NAME<64, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 63) / 64), block, 0,   \
                          s, a);                                                                          \
       break;                                                                                             \
   }
     switch (R) {
-      case R_QKV_FWD: RG_LAUNCH(gemm_qkv_fwd) break;
-      case R_O_FWD: RG_LAUNCH(gemm_o_fwd) break;
-      case R_FFN_IN_FWD: RG_LAUNCH(gemm_ffn_in_fwd) break;
-      case R_FFN_OUT_FWD: RG_LAUNCH(gemm_ffn_out_fwd) break;
-      case R_QKV_DX: RG_LAUNCH(gemm_qkv_dx) break;
-      case R_O_DX: RG_LAUNCH(gemm_o_dx) break;
-      case R_FFN_IN_DX: RG_LAUNCH(gemm_ffn_in_dx) break;
-      case R_FFN_OUT_DX: RG_LAUNCH(gemm_ffn_out_dx) break;
+      case R_QKV_FWD: RG_LAUNCH_CFG(gemm_qkv_fwd) break;
+      case R_O_FWD: RG_LAUNCH_CFG(gemm_o_fwd) break;
+      case R_FFN_IN_FWD: RG_LAUNCH_CFG(gemm_ffn_in_fwd) break;
+      case R_FFN_OUT_FWD: RG_LAUNCH_CFG(gemm_ffn_out_fwd) break;
+      case R_QKV_DX: RG_LAUNCH_CFG(gemm_qkv_dx) break;
+      case R_O_DX: RG_LAUNCH_CFG(gemm_o_dx) break;
+      case R_FFN_IN_DX: RG_LAUNCH_CFG(gemm_ffn_in_dx) break;
+      case R_FFN_OUT_DX: RG_LAUNCH_CFG(gemm_ffn_out_dx) break;
       default: return hipErrorInvalidValue;
     }
-#undef RG_LAUNCH
+#undef RG_LAUNCH_CFG
 #undef RG_TILES
 #undef RG_NAME
     return hipGetLastError();

@@ -57,10 +57,10 @@ hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, con
   if (T < 0 || d <= 0 || !x || !g || !out) return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(rms_fwd_k<bf16>, dim3(T), dim3(256), 0, s, d, eps, (const bf16*)x,
+    RG_LAUNCH(rms_fwd_k<bf16>, dim3(T), dim3(256), 0, s, d, eps, (const bf16*)x,
                        (const bf16*)g, (bf16*)out, (bf16*)xhat, rstd);
   else
-    hipLaunchKernelGGL(rms_fwd_k<float>, dim3(T), dim3(256), 0, s, d, eps, (const float*)x,
+    RG_LAUNCH(rms_fwd_k<float>, dim3(T), dim3(256), 0, s, d, eps, (const float*)x,
                        (const float*)g, (float*)out, (float*)xhat, rstd);
   return hipGetLastError();
 }
@@ -70,10 +70,10 @@ hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* d
   if (T < 0 || d <= 0 || !dn || !dres || !xhat || !rstd || !g || !dx) return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(rms_bwd_k<bf16>, dim3(T), dim3(256), 0, s, d, (const bf16*)dn,
+    RG_LAUNCH(rms_bwd_k<bf16>, dim3(T), dim3(256), 0, s, d, (const bf16*)dn,
                        (const bf16*)dres, (const bf16*)xhat, rstd, (const bf16*)g, (bf16*)dx);
   else
-    hipLaunchKernelGGL(rms_bwd_k<float>, dim3(T), dim3(256), 0, s, d, (const float*)dn,
+    RG_LAUNCH(rms_bwd_k<float>, dim3(T), dim3(256), 0, s, d, (const float*)dn,
                        (const float*)dres, (const float*)xhat, rstd, (const float*)g, (float*)dx);
   return hipGetLastError();
 }
@@ -99,11 +99,11 @@ hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int row
   if (!in || !out || rows <= 0 || cols <= 0) return hipErrorInvalidValue;
   const dim3 grid((cols + 31) / 32, (rows + 31) / 32), block(256);
   if (in_dtype == DT_F32 && out_dtype == DT_F32)
-    hipLaunchKernelGGL((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out);
+    RG_LAUNCH((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out);
   else if (in_dtype == DT_F32 && out_dtype == DT_BF16)
-    hipLaunchKernelGGL((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out);
+    RG_LAUNCH((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out);
   else if (in_dtype == DT_BF16 && out_dtype == DT_BF16)
-    hipLaunchKernelGGL((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out);
+    RG_LAUNCH((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -123,8 +123,8 @@ __global__ __launch_bounds__(256) void pack_swiglu_k(const T* wgu, int d, int F,
 hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s) {
   if (!w_gu || !out || d <= 0 || F <= 0 || F % 32) return hipErrorInvalidValue;
   const dim3 grid(4096), block(256);
-  if (dtype == DT_BF16) hipLaunchKernelGGL(pack_swiglu_k<bf16>, grid, block, 0, s, (const bf16*)w_gu, d, F, (bf16*)out);
-  else hipLaunchKernelGGL(pack_swiglu_k<float>, grid, block, 0, s, (const float*)w_gu, d, F, (float*)out);
+  if (dtype == DT_BF16) RG_LAUNCH(pack_swiglu_k<bf16>, grid, block, 0, s, (const bf16*)w_gu, d, F, (bf16*)out);
+  else RG_LAUNCH(pack_swiglu_k<float>, grid, block, 0, s, (const float*)w_gu, d, F, (float*)out);
   return hipGetLastError();
 }
 
@@ -168,8 +168,8 @@ static hipError_t adapter_update(int dtype, const AdapterSlot* slots, int n_slot
   if (n_slots == 0) return hipSuccess;
   const long n = 2L * d * m;
   const dim3 grid((unsigned)((n + 255) / 256 < 256 ? (n + 255) / 256 : 256), n_slots), block(256);
-  if (dtype == DT_BF16) hipLaunchKernelGGL((adapter_update_k<bf16, UPDATE>), grid, block, 0, s, slots, d, m, lr);
-  else hipLaunchKernelGGL((adapter_update_k<float, UPDATE>), grid, block, 0, s, slots, d, m, lr);
+  if (dtype == DT_BF16) RG_LAUNCH((adapter_update_k<bf16, UPDATE>), grid, block, 0, s, slots, d, m, lr);
+  else RG_LAUNCH((adapter_update_k<float, UPDATE>), grid, block, 0, s, slots, d, m, lr);
   return hipGetLastError();
 }
 
@@ -199,8 +199,8 @@ __global__ __launch_bounds__(1024) void mse_k(const T* y, const T* t, long n, T*
 
 hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy, float* loss, hipStream_t s) {
   if (!y || !t || !dy || n <= 0) return hipErrorInvalidValue;
-  if (dtype == DT_BF16) hipLaunchKernelGGL(mse_k<bf16>, dim3(1), dim3(1024), 0, s, (const bf16*)y, (const bf16*)t, n, (bf16*)dy, loss);
-  else hipLaunchKernelGGL(mse_k<float>, dim3(1), dim3(1024), 0, s, (const float*)y, (const float*)t, n, (float*)dy, loss);
+  if (dtype == DT_BF16) RG_LAUNCH(mse_k<bf16>, dim3(1), dim3(1024), 0, s, (const bf16*)y, (const bf16*)t, n, (bf16*)dy, loss);
+  else RG_LAUNCH(mse_k<float>, dim3(1), dim3(1024), 0, s, (const float*)y, (const float*)t, n, (float*)dy, loss);
   return hipGetLastError();
 }
 
@@ -321,10 +321,10 @@ hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const f
   const long zero_rows = (long)B * (S - 1);
   const dim3 grid(1 + (unsigned)(zero_rows < 1024 ? zero_rows : 1024)), block(256);
   if (dtype == DT_BF16)
-    hipLaunchKernelGGL(head_ce_k<bf16>, grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
+    RG_LAUNCH(head_ce_k<bf16>, grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
                        (bf16*)dy, gwh, gbh, loss);
   else
-    hipLaunchKernelGGL(head_ce_k<float>, grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels,
+    RG_LAUNCH(head_ce_k<float>, grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels,
                        (float*)dy, gwh, gbh, loss);
   return hipGetLastError();
 }
@@ -339,7 +339,7 @@ __global__ __launch_bounds__(256) void sgd_f32_k(float* w, float* g, long n, flo
 hipError_t launch_sgd_f32(float* w, float* g, long n, float lr, hipStream_t s) {
   if (!w || !g || n <= 0) return hipErrorInvalidValue;
   const long nb = (n + 255) / 256;
-  hipLaunchKernelGGL(sgd_f32_k, dim3((unsigned)(nb < 1024 ? nb : 1024)), dim3(256), 0, s, w, g, n, lr);
+  RG_LAUNCH(sgd_f32_k, dim3((unsigned)(nb < 1024 ? nb : 1024)), dim3(256), 0, s, w, g, n, lr);
   return hipGetLastError();
 }
 

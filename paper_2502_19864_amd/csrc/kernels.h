@@ -1,9 +1,31 @@
 // Host-side launchers of the RingAda kernels (internal to libringada).
 #pragma once
+#include <hip/hip_ext.h>
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
 namespace rg {
+
+// Optional timing of the next launches: when set (by the stage's profiling
+// pass, never under graph capture), RG_LAUNCH goes through the HIP extension
+// launch, which timestamps the kernel's own dispatch (start on the first
+// launch, stop on every launch, so the pair spans all kernels of one call).
+struct LaunchEvents {
+  hipEvent_t start, stop;
+  bool started;
+};
+extern thread_local LaunchEvents* g_launch_events;
+
+#define RG_LAUNCH(K, G, B, SH, S, ...)                                                            \
+  do {                                                                                            \
+    if (::rg::LaunchEvents* le_ = ::rg::g_launch_events) {                                        \
+      hipExtLaunchKernelGGL(K, G, B, SH, S, le_->started ? nullptr : le_->start, le_->stop, 0,    \
+                            __VA_ARGS__);                                                         \
+      le_->started = true;                                                                        \
+    } else {                                                                                      \
+      hipLaunchKernelGGL(K, G, B, SH, S, __VA_ARGS__);                                            \
+    }                                                                                             \
+  } while (0)
 
 enum { DT_F32 = 0, DT_BF16 = 1 };
 

@@ -335,6 +335,8 @@ extern "C" ringada_status ringada_stage_sync_adapters(ringada_stage* st, void* s
 }
 
 // ================================================================ launches (with optional event timing)
+thread_local LaunchEvents* rg::g_launch_events = nullptr;
+
 static hipEvent_t pool_event(ringada_stage* st) {
   if (st->evused == st->evpool.size()) {
     hipEvent_t e;
@@ -346,19 +348,20 @@ static hipEvent_t pool_event(ringada_stage* st) {
 
 template <class Fn>
 static ringada_status run(ringada_stage* st, hipStream_t s, const char* name, double flops, double bytes, Fn&& fn) {
-  hipEvent_t e0 = nullptr, e1 = nullptr;
-  if (st->prof) {
-    e0 = pool_event(st);
-    e1 = pool_event(st);
-    if (!e0 || !e1) return fail(RINGADA_E_HIP, "hipEventCreate failed");
-    RG_HIP(hipEventRecord(e0, s));
+  if (!st->prof) {
+    const hipError_t e = fn();
+    if (e != hipSuccess) return fail(RINGADA_E_HIP, "%s: %s", name, hipGetErrorString(e));
+    return RINGADA_OK;
   }
+  // the launches inside fn() carry the events (kernel start .. kernel end)
+  LaunchEvents le{pool_event(st), pool_event(st), false};
+  if (!le.start || !le.stop) return fail(RINGADA_E_HIP, "hipEventCreate failed");
+  g_launch_events = &le;
   const hipError_t e = fn();
+  g_launch_events = nullptr;
   if (e != hipSuccess) return fail(RINGADA_E_HIP, "%s: %s", name, hipGetErrorString(e));
-  if (st->prof) {
-    RG_HIP(hipEventRecord(e1, s));
-    st->recs.push_back(ProfRec{name, flops, bytes, e0, e1});
-  }
+  if (!le.started) return RINGADA_OK;  // nothing launched (empty input)
+  st->recs.push_back(ProfRec{name, flops, bytes, le.start, le.stop});
   return RINGADA_OK;
 }
 
