@@ -83,7 +83,7 @@ def cpu_baseline(w, inp):
     import oracle as O
     from threadpoolctl import threadpool_info
     from paper_2502_19864_amd.workloads import adapters_as_computed
-    desc = O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter)
+    desc = O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter, placement=w.placement)
     W = inp["weights"]
     A = adapters_as_computed(w, inp["adapters"])
     t0 = time.perf_counter()

@@ -32,7 +32,11 @@ Readings where the paper is silent (each is listed in the design notes):
   * sigma in Eq. (1) is GELU in its exact erf form;
   * an adapter acts on its sublayer's output before the block's residual
     add (and before the LayerNorm in post-LN blocks);
-  * two adapters per block (Houlsby placement); both unfreeze together;
+  * two adapters per block (Houlsby placement); both unfreeze together.
+    The single serial placement of Sec. II-A (Fig. 1: one adapter, after the
+    feed-forward sublayer) is the option placement='ffn': the attention
+    sublayer then carries no adapter, and the backward of the lowest
+    unfrozen block ends after that block's FFN-adapter weight gradients;
   * adapters have no biases, exactly as in Eq. (1);
   * weights are stored [in, out] so a projection is ``x @ W`` as in Eq. (1);
   * the unfreezing cut-off of Alg. 1 uses L = total number of Trm blocks.
@@ -188,14 +192,21 @@ def rope_bwd(dy, cos, sin):
 # stage description
 # --------------------------------------------------------------------------
 def make_desc(arch, n_blocks, d_model, n_heads, d_ffn, d_adapter,
-              norm_eps=None, rope_theta=10000.0):
+              norm_eps=None, rope_theta=10000.0, placement="houlsby"):
     """arch is 'bert' (post-LN, GELU FFN, bidirectional) or 'llama'
-    (pre-RMSNorm, SwiGLU FFN, RoPE, causal)."""
+    (pre-RMSNorm, SwiGLU FFN, RoPE, causal).  placement is 'houlsby' (an
+    adapter on the attention and on the FFN sublayer of every block) or
+    'ffn' (the single adapter after the feed-forward sublayer, Sec. II-A)."""
     if norm_eps is None:
         norm_eps = 1e-12 if arch == "bert" else 1e-6
+    assert placement in ("houlsby", "ffn")
     return dict(arch=arch, n_blocks=n_blocks, d_model=d_model, n_heads=n_heads,
                 d_ffn=d_ffn, d_adapter=d_adapter, norm_eps=norm_eps,
-                rope_theta=rope_theta)
+                rope_theta=rope_theta, placement=placement)
+
+
+def _single(desc):
+    return desc.get("placement", "houlsby") == "ffn"
 
 
 # --------------------------------------------------------------------------
@@ -212,7 +223,10 @@ def bert_block_fwd(desc, w, ad, x, B, S):
     o_h, p = attention_fwd(q, k, v, causal=False)
     o = merge_heads(o_h)
     attn = o @ w["w_o"] + w["b_o"]
-    a, u1 = adapter_fwd(attn, ad[0]["w_down"], ad[0]["w_up"])
+    if _single(desc):
+        a, u1 = attn, None
+    else:
+        a, u1 = adapter_fwd(attn, ad[0]["w_down"], ad[0]["w_up"])
     h1, xhat1, rstd1 = layer_norm(x + a, w["ln1_g"], w["ln1_b"], eps)
     a1 = h1 @ w["w_i"] + w["b_i"]
     f2 = gelu(a1) @ w["w_f"] + w["b_f"]
@@ -224,19 +238,29 @@ def bert_block_fwd(desc, w, ad, x, B, S):
 
 
 def bert_block_bwd(desc, w, ad, c, dy, B, S, stop):
-    """Backward of one post-LN block.  Returns (dx or None, adapter grads).
-    With stop=True the pass ends after the attention adapter's weight
-    gradients: no gradient reaches the block input."""
+    """Backward of one post-LN block.  Returns (dx or None, adapter grads),
+    grads = (attention adapter or None, FFN adapter).  With stop=True the
+    pass ends after the weight gradients of the block's lowest adapter (the
+    attention adapter; the FFN adapter under the single placement): no
+    gradient reaches the block input."""
+    single = _single(desc)
     dz2 = layer_norm_bwd(dy, w["ln2_g"], c["xhat2"], c["rstd2"])
     df2, gdn2, gup2 = adapter_bwd(dz2, c["f2"], c["u2"],
-                                  ad[1]["w_down"], ad[1]["w_up"])
+                                  ad[1]["w_down"], ad[1]["w_up"],
+                                  need_dh=not (single and stop))
+    g_ffn = {"w_down": gdn2, "w_up": gup2}
+    if single and stop:
+        return None, (None, g_ffn)
     da1 = (df2 @ w["w_f"].T) * gelu_grad(c["a1"])
     dh1 = dz2 + da1 @ w["w_i"].T
     dz1 = layer_norm_bwd(dh1, w["ln1_g"], c["xhat1"], c["rstd1"])
-    dattn, gdn1, gup1 = adapter_bwd(dz1, c["attn"], c["u1"],
-                                    ad[0]["w_down"], ad[0]["w_up"],
-                                    need_dh=not stop)
-    grads = ({"w_down": gdn1, "w_up": gup1}, {"w_down": gdn2, "w_up": gup2})
+    if single:
+        dattn, grads = dz1, (None, g_ffn)
+    else:
+        dattn, gdn1, gup1 = adapter_bwd(dz1, c["attn"], c["u1"],
+                                        ad[0]["w_down"], ad[0]["w_up"],
+                                        need_dh=not stop)
+        grads = ({"w_down": gdn1, "w_up": gup1}, g_ffn)
     if stop:
         return None, grads
     do = split_heads(dattn @ w["w_o"].T, B, S, desc["n_heads"])
@@ -262,7 +286,10 @@ def llama_block_fwd(desc, w, ad, x, B, S):
     v = split_heads(qkv[:, 2 * d:], B, S, H)
     o_h, p = attention_fwd(q, k, v, causal=True)
     attn = merge_heads(o_h) @ w["w_o"]
-    a, u1 = adapter_fwd(attn, ad[0]["w_down"], ad[0]["w_up"])
+    if _single(desc):
+        a, u1 = attn, None
+    else:
+        a, u1 = adapter_fwd(attn, ad[0]["w_down"], ad[0]["w_up"])
     h = x + a
     n2, xhat2, rstd2 = rms_norm(h, w["rms2_g"], eps)
     gu = n2 @ w["w_gu"]
@@ -278,18 +305,26 @@ def llama_block_fwd(desc, w, ad, x, B, S):
 
 def llama_block_bwd(desc, w, ad, c, dy, B, S, stop):
     F, H = desc["d_ffn"], desc["n_heads"]
+    single = _single(desc)
     dh_res = dy
     df, gdn2, gup2 = adapter_bwd(dy, c["f"], c["u2"],
-                                 ad[1]["w_down"], ad[1]["w_up"])
+                                 ad[1]["w_down"], ad[1]["w_up"],
+                                 need_dh=not (single and stop))
+    g_ffn = {"w_down": gdn2, "w_up": gup2}
+    if single and stop:
+        return None, (None, g_ffn)
     dact = df @ w["w_d"].T
     dgate = dact * c["up"] * silu_grad(c["gate"])
     dup = dact * silu(c["gate"])
     dn2 = np.concatenate([dgate, dup], axis=1) @ w["w_gu"].T
     dh = dh_res + rms_norm_bwd(dn2, w["rms2_g"], c["xhat2"], c["rstd2"])
-    dattn, gdn1, gup1 = adapter_bwd(dh, c["attn"], c["u1"],
-                                    ad[0]["w_down"], ad[0]["w_up"],
-                                    need_dh=not stop)
-    grads = ({"w_down": gdn1, "w_up": gup1}, {"w_down": gdn2, "w_up": gup2})
+    if single:
+        dattn, grads = dh, (None, g_ffn)
+    else:
+        dattn, gdn1, gup1 = adapter_bwd(dh, c["attn"], c["u1"],
+                                        ad[0]["w_down"], ad[0]["w_up"],
+                                        need_dh=not stop)
+        grads = ({"w_down": gdn1, "w_up": gup1}, g_ffn)
     if stop:
         return None, grads
     do = split_heads(dattn @ w["w_o"].T, B, S, H)
@@ -329,10 +364,13 @@ def stage_backward(desc, weights, adapters, caches, dy, lowest_unfrozen):
       c < 0       every local adapter is unfrozen; the gradient w.r.t. the
                   stage input is returned (the cut-off is upstream);
       0 <= c < L  blocks c..L-1 have unfrozen adapters; the pass ends after
-                  the weight gradients of block c's attention adapter;
+                  the weight gradients of block c's lowest adapter (its
+                  attention adapter, or its FFN adapter under the single
+                  placement);
       c >= L      all adapters frozen: no backward at all.
     Returns (dx_in or None, grads) with grads[l] = (attn, ffn) dicts for the
-    unfrozen blocks and None for the frozen ones.
+    unfrozen blocks (attn is None under the single placement) and None for
+    the frozen ones.
     """
     B, S, d = dy.shape
     L = desc["n_blocks"]
@@ -358,7 +396,7 @@ def sgd_step(adapters, grads, lr):
         if gr is None:
             out.append(ad)
             continue
-        out.append(tuple({k: a[k] - lr * g[k] for k in ("w_down", "w_up")}
+        out.append(tuple(a if g is None else {k: a[k] - lr * g[k] for k in ("w_down", "w_up")}
                          for a, g in zip(ad, gr)))
     return out
 

@@ -57,6 +57,7 @@ class Workload:
     loss: str            # 'mse' | 'cls_ce' | 'dy'
     seed: int
     tiny_adapter_init: bool = False
+    placement: str = "houlsby"  # or 'ffn': one adapter per block, after the FFN
 
     def replace(self, **kw):
         return dataclasses.replace(self, **kw)
@@ -86,6 +87,11 @@ WORKLOADS = {
     # batch 4, top 2 blocks unfrozen, incoming dY ~ N(0, 1e-2).
     "llama7b_share": Workload("llama7b_share", "llama", "bf16", 8, 4096, 32,
                               11008, 64, 512, 4, 6, "dy", 1005),
+    # bert_base with the single serial adapter per block (after the FFN
+    # sublayer, as in the paper's own set-up), cut-off at block 8.
+    "bert_base_single": Workload("bert_base_single", "bert", "bf16", 12, 768,
+                                 12, 3072, 64, 128, 32, 8, "cls_ce", 1006,
+                                 placement="ffn"),
 }
 SWEEP = (11, 9, 6, 3, 0)
 

@@ -74,8 +74,11 @@ def bert_block_fwd_bf16(desc, w, ad, x, B, S):
     e_ = np.exp(s_ - s_.max(axis=-1, keepdims=True))
     o_h = (_rb(e_) @ v) / e_.sum(axis=-1, keepdims=True)
     attn = _rb(_rb(O.merge_heads(o_h)) @ w["w_o"] + w["b_o"])
-    U1 = attn @ ad[0]["w_down"]
-    a = attn + _rb(O.gelu(U1)) @ ad[0]["w_up"]
+    if desc.get("placement", "houlsby") == "ffn":
+        U1, a = None, attn
+    else:
+        U1 = attn @ ad[0]["w_down"]
+        a = attn + _rb(O.gelu(U1)) @ ad[0]["w_up"]
     h1, xhat1, rstd1 = O.layer_norm(x + a, w["ln1_g"], w["ln1_b"], eps)
     h1 = _rb(h1)
     A1 = h1 @ w["w_i"] + w["b_i"]
@@ -83,7 +86,8 @@ def bert_block_fwd_bf16(desc, w, ad, x, B, S):
     U2 = f2 @ ad[1]["w_down"]
     fa = f2 + _rb(O.gelu(U2)) @ ad[1]["w_up"]
     y, xhat2, rstd2 = O.layer_norm(h1 + fa, w["ln2_g"], w["ln2_b"], eps)
-    cache = dict(q=q, k=k, v=v, p=p, attn=attn, u1=_rb(U1), xhat1=_rb(xhat1), rstd1=rstd1, a1=_rb(A1),
+    cache = dict(q=q, k=k, v=v, p=p, attn=attn, u1=None if U1 is None else _rb(U1), xhat1=_rb(xhat1), rstd1=rstd1,
+                 a1=_rb(A1),
                  f2=f2, u2=_rb(U2), xhat2=_rb(xhat2), rstd2=rstd2)
     return _rb(y), cache
 
@@ -117,6 +121,8 @@ def bert_floor(w, inp, c, ref):
     _, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
     for l in range(max(c, 0), w.n_blocks):
         for a in range(2):
+            if g_emu[l][a] is None:
+                continue
             for k in ("w_down", "w_up"):
                 out[(l, a, k)] = rel_err(g_emu[l][a][k], ref["grads"][l][a][k])
     return out

@@ -20,7 +20,7 @@ def rel_err(got, ref):
 
 
 def oracle_desc(w):
-    return O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter)
+    return O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter, placement=w.placement)
 
 
 def to64(inp, w):

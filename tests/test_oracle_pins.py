@@ -15,14 +15,23 @@ from paper_2502_19864_amd.workloads import WORKLOADS, make_inputs
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
-def _tiny_bert(seed=7, B=2, S=5, d=16, H=2, F=24, m=4, L=2):
-    desc = O.make_desc("bert", L, d, H, F, m)
+def _tiny_bert(seed=7, B=2, S=5, d=16, H=2, F=24, m=4, L=2, placement="houlsby"):
+    desc = O.make_desc("bert", L, d, H, F, m, placement=placement)
     return desc, _rand_params(desc, seed, B, S)
 
 
-def _tiny_llama(seed=8, B=2, S=6, d=16, H=2, F=20, m=4, L=2):
-    desc = O.make_desc("llama", L, d, H, F, m)
+def _tiny_llama(seed=8, B=2, S=6, d=16, H=2, F=20, m=4, L=2, placement="houlsby"):
+    desc = O.make_desc("llama", L, d, H, F, m, placement=placement)
     return desc, _rand_params(desc, seed, B, S)
+
+
+def _tiny(arch, placement="houlsby", **kw):
+    return (_tiny_bert if arch == "bert" else _tiny_llama)(placement=placement, **kw)
+
+
+def _adapters_of(placement):
+    """indices of the adapters a block carries: (attention, FFN) or FFN only"""
+    return (0, 1) if placement == "houlsby" else (1,)
 
 
 def _rand_params(desc, seed, B, S):
@@ -198,9 +207,10 @@ def _loss_and_grads(desc, weights, adapters, x, dy, c):
     return (y * dy).sum(), dx, grads
 
 
+@pytest.mark.parametrize("placement", ["houlsby", "ffn"])
 @pytest.mark.parametrize("arch", ["bert", "llama"])
-def test_stage_gradients_by_central_differences(arch):
-    desc, p = _tiny_bert() if arch == "bert" else _tiny_llama()
+def test_stage_gradients_by_central_differences(arch, placement):
+    desc, p = _tiny(arch, placement)
     W, A, x, dy = p["weights"], p["adapters"], p["x"], p["dy"]
     _, dx, grads = _loss_and_grads(desc, W, A, x, dy, -1)
     rng = np.random.default_rng(11)
@@ -211,7 +221,9 @@ def test_stage_gradients_by_central_differences(arch):
         return (y * dy).sum()
 
     for l in range(desc["n_blocks"]):
-        for a in range(2):
+        if placement == "ffn":
+            assert grads[l][0] is None
+        for a in _adapters_of(placement):
             for name in ("w_down", "w_up"):
                 g = grads[l][a][name]
                 scale = np.abs(g).max()
@@ -235,11 +247,12 @@ def test_stage_gradients_by_central_differences(arch):
         assert abs(fd - dx[idx]) <= 1e-6 * scale
 
 
+@pytest.mark.parametrize("placement", ["houlsby", "ffn"])
 @pytest.mark.parametrize("arch", ["bert", "llama"])
-def test_truncated_backward_equals_full_backward(arch):
+def test_truncated_backward_equals_full_backward(arch, placement):
     """Early stopping at block c leaves every produced gradient bitwise equal
     to the full backward's and produces nothing below c."""
-    desc, p = (_tiny_bert(L=4) if arch == "bert" else _tiny_llama(L=4))
+    desc, p = _tiny(arch, placement, L=4)
     W, A, x, dy = p["weights"], p["adapters"], p["x"], p["dy"]
     _, dx_full, g_full = _loss_and_grads(desc, W, A, x, dy, -1)
     assert dx_full is not None
@@ -250,9 +263,38 @@ def test_truncated_backward_equals_full_backward(arch):
             if l < c:
                 assert g[l] is None
             else:
-                for a in range(2):
+                for a in _adapters_of(placement):
                     for k in ("w_down", "w_up"):
                         assert np.array_equal(g[l][a][k], g_full[l][a][k])
+
+
+@pytest.mark.parametrize("arch", ["bert", "llama"])
+def test_single_placement_is_houlsby_without_the_attention_adapter(arch):
+    """The single placement equals the two-adapter stage whose attention
+    adapters have W_up = 0 (Eq. (1) is then the identity): the same output,
+    the same input gradient and the same FFN-adapter gradients, bitwise; and
+    the attention adapter's W_down gets no gradient there."""
+    d1, p = _tiny(arch, "ffn", L=3)
+    d2 = dict(d1, placement="houlsby")
+    W, x, dy = p["weights"], p["x"], p["dy"]
+    A0 = [({"w_down": pair[0]["w_down"], "w_up": np.zeros_like(pair[0]["w_up"])}, pair[1])
+          for pair in p["adapters"]]
+    l1, dx1, g1 = _loss_and_grads(d1, W, p["adapters"], x, dy, -1)
+    l2, dx2, g2 = _loss_and_grads(d2, W, A0, x, dy, -1)
+    assert l1 == l2
+    assert np.array_equal(O.stage_forward(d1, W, p["adapters"], x)[0], O.stage_forward(d2, W, A0, x)[0])
+    assert np.array_equal(dx1, dx2)
+    for l in range(3):
+        assert g1[l][0] is None
+        assert np.all(g2[l][0]["w_down"] == 0)
+        for k in ("w_down", "w_up"):
+            assert np.array_equal(g1[l][1][k], g2[l][1][k])
+    # the single placement stops one sublayer earlier: at c the FFN adapter's
+    # gradients are the last thing produced, and they match the full pass
+    for c in range(3):
+        _, _, g = _loss_and_grads(d1, W, p["adapters"], x, dy, c)
+        for k in ("w_down", "w_up"):
+            assert np.array_equal(g[c][1][k], g1[c][1][k])
 
 
 def test_causality_and_batch_independence():
