@@ -241,6 +241,7 @@ def main():
                                f"blocks, d={w.d_model}, {w.n_heads} heads, FFN {w.d_ffn}, two adapters/block "
                                f"m={w.d_adapter}, seq {w.seq}, batch {w.batch}, lowest unfrozen block {c}",
                    "batch": w.batch, "seq_len": w.seq, "n_blocks": w.n_blocks, "lowest_unfrozen": c,
+                   "placement": w.placement,
                    "parallelism": "one ring stage on one GPU"},
         "tokens_per_s": round(value * w.seq, 1),
         "gemm_mfma_frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,

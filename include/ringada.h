@@ -63,6 +63,14 @@ enum {
   RINGADA_ARCH_PRERMS_SWIGLU = 1
 };
 enum { RINGADA_F32 = 0, RINGADA_BF16 = 1 };
+enum {
+  /* two adapters per block: one on the attention sublayer's output, one on
+   * the FFN sublayer's output, each before the block's residual add */
+  RINGADA_PLACEMENT_HOULSBY = 0,
+  /* the single serial adapter of Sec. II-A (Fig. 1): one adapter per block,
+   * on the FFN sublayer's output; the attention sublayer carries none */
+  RINGADA_PLACEMENT_FFN = 1
+};
 
 typedef struct {
   int32_t arch;       /* RINGADA_ARCH_* */
@@ -77,6 +85,7 @@ typedef struct {
   int32_t max_seq;
   float norm_eps;     /* LayerNorm / RMSNorm epsilon (added to the variance) */
   float rope_theta;   /* RoPE base, pre-RMS arch only */
+  int32_t placement;  /* RINGADA_PLACEMENT_*: where the adapters sit */
 } ringada_stage_desc;
 
 /* Frozen weights of one block, device pointers in the stage dtype, all
@@ -148,8 +157,9 @@ int32_t ringada_local_cutoff(int32_t n_tm, int32_t depth, int32_t first_block,
 ringada_status ringada_stage_create(const ringada_stage_desc* desc,
                                     ringada_stage** out);
 
-/* Binds block `block` (0-indexed, local).  Frozen weights and both adapters are
- * borrowed.  The library allocates, on the current device, a transposed copy
+/* Binds block `block` (0-indexed, local).  Frozen weights and the adapters
+ * are borrowed; under RINGADA_PLACEMENT_FFN attn_adapter must be NULL (the
+ * block has none), otherwise both are required.  The library allocates, on the current device, a transposed copy
  * of each frozen projection matrix (the forward multiplies by it; the frozen
  * weights never change, so the copy stays valid) and working copies of the
  * adapters in the stage dtype, fills them on `stream` and synchronises the
@@ -185,9 +195,11 @@ ringada_status ringada_stage_forward(ringada_stage* st, void* stream,
 /* Early-stopped backward of the pending forward.  dy [batch, seq, d] is the
  * gradient at the stage output.  For blocks l >= max(c, 0), from the top
  * down: activation gradients through the frozen weights (no frozen weight
- * gradient is formed) and both adapters' weight gradients, ADDED into their
- * g_down / g_up.  With 0 <= c < n_blocks the pass ends after the attention
- * adapter of block c (its weight gradients are the last thing computed);
+ * gradient is formed) and the adapters' weight gradients, ADDED into their
+ * g_down / g_up.  With 0 <= c < n_blocks the pass ends after the lowest
+ * adapter of block c (its weight gradients are the last thing computed):
+ * the attention adapter, or under RINGADA_PLACEMENT_FFN the FFN adapter, so
+ * that block's FFN, norms and attention are not back-propagated at all;
  * with c < 0 the gradient w.r.t. the stage input is written to dx_in.
  * dx_in must be non-NULL iff c < 0.  c must be >= the forward's cut-off
  * (else RINGADA_E_STATE: the stash does not reach that deep), and < n_blocks.

@@ -13,6 +13,7 @@ LIB_PATH = os.path.join(_HERE, "libringada.so")
 RINGADA_OK, RINGADA_E_INVALID, RINGADA_E_STATE, RINGADA_E_WORKSPACE, RINGADA_E_UNSUPPORTED, RINGADA_E_HIP = range(6)
 ARCH_POSTLN_GELU, ARCH_PRERMS_SWIGLU = 0, 1
 F32, BF16 = 0, 1
+PLACEMENT_HOULSBY, PLACEMENT_FFN = 0, 1
 STATUS_NAMES = {0: "OK", 1: "E_INVALID", 2: "E_STATE", 3: "E_WORKSPACE", 4: "E_UNSUPPORTED", 5: "E_HIP"}
 
 
@@ -26,7 +27,7 @@ class StageDesc(ctypes.Structure):
     _fields_ = [("arch", c_int32), ("dtype", c_int32), ("n_blocks", c_int32), ("d_model", c_int32),
                 ("n_heads", c_int32), ("d_ffn", c_int32), ("d_adapter", c_int32),
                 ("max_batch", c_int32), ("max_seq", c_int32), ("norm_eps", c_float),
-                ("rope_theta", c_float)]
+                ("rope_theta", c_float), ("placement", c_int32)]
 
 
 class BlockWeights(ctypes.Structure):
@@ -121,7 +122,9 @@ def ringada_stage_create(desc):
 
 
 def ringada_stage_bind_block(stage, block, frozen, attn_adapter, ffn_adapter, stream):
-    _check(lib().ringada_stage_bind_block(stage, block, byref(frozen), byref(attn_adapter),
+    """attn_adapter is None for a stage with the single (FFN) placement."""
+    _check(lib().ringada_stage_bind_block(stage, block, byref(frozen),
+                                          None if attn_adapter is None else byref(attn_adapter),
                                           byref(ffn_adapter), stream))
 
 

@@ -41,6 +41,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   const long trow = (long)(tv ? token : 0) * D;
   const bf16* z = static_cast<const bf16*>(a.z);
   const int f0 = wave * 16 * FB;
+  const bool has_ad = a.wdn_t != nullptr;  // else: residual add + norm only
 
   // z tile -> LDS
   {
@@ -70,16 +71,18 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   bf16x8 w0[FB], w1[FB];
   const bf16* wu = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
   if constexpr (PRE) {
+    if (has_ad) {
 #pragma unroll
-    for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(wu + (long)b * 16 * MB);
-      w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+      for (int b = 0; b < FB; ++b) {
+        w0[b] = ld_frag(wu + (long)b * 16 * MB);
+        w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+      }
     }
   }
   __syncthreads();
 
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:]
-  {
+  if (has_ad) {
     const int ug = wave % 4, ks = wave / 4;
     const bf16* wd = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
     const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
@@ -121,19 +124,27 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  + z + res
   float v[FB][4];
   {
-    const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+    bf16x8 g0 = zero_frag(), g1 = zero_frag();
+    if (has_ad) {
+      g0 = ld_frag(sG + l16 * GP + 8 * grp);
+      g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+    }
     if constexpr (!PRE) {
+      if (has_ad) {
 #pragma unroll
-      for (int b = 0; b < FB; ++b) {
-        w0[b] = ld_frag(wu + (long)b * 16 * MB);
-        w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+        for (int b = 0; b < FB; ++b) {
+          w0[b] = ld_frag(wu + (long)b * 16 * MB);
+          w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+        }
       }
     }
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
       f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      acc = mfma16(w0[b], g0, acc);
-      acc = mfma16(w1[b], g1, acc);
+      if (has_ad) {
+        acc = mfma16(w0[b], g0, acc);
+        acc = mfma16(w1[b], g1, acc);
+      }
       float zz[4];
       St<bf16>::ld4(sZ, l16 * DP + f0 + b * 16 + 4 * grp, zz);
       const float r4[4] = {__uint_as_float(rr[b].x << 16), __uint_as_float(rr[b].x & 0xffff0000u),
@@ -234,16 +245,17 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
     zv[i] = (c < NCH && t0 + r < T) ? *reinterpret_cast<const uint4*>(z + (long)(t0 + r) * D + k)
                                     : make_uint4(0, 0, 0, 0);
   }
+  const bool has_ad = a.wdn_t != nullptr;  // else: residual add + norm only
   const int ug = wave % 4, ks = wave / 4;
   bf16x8 wd[NSTEP];
-  {
+  if (has_ad) {
     const bf16* p = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
 #pragma unroll
     for (int j = 0; j < NSTEP; ++j) wd[j] = ld_frag(p + j * 32);
   }
   const int f0 = wave * 16 * FB;
   bf16x8 w0[FB], w1[FB];
-  {
+  if (has_ad) {
     const bf16* p = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
@@ -267,7 +279,7 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   __syncthreads();
 
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:], k split over KS waves
-  {
+  if (has_ad) {
     const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
     f32x4 u = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -288,11 +300,11 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
       if (a.u && t0 + l16 < T) St<bf16>::st4(static_cast<bf16*>(a.u), (long)(t0 + l16) * MB + ug * 16 + 4 * grp, uv);
       St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  -> sV (fp32)
-  {
+  if (has_ad) {
     const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
@@ -301,8 +313,8 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
       acc = mfma16(w1[b], g1, acc);
       *reinterpret_cast<float4*>(sV + l16 * VP + f0 + b * 16 + 4 * grp) = make_float4(acc[0], acc[1], acc[2], acc[3]);
     }
+    __syncthreads();
   }
-  __syncthreads();
 
   // ---- add + norm, wave = token
   if (!twv) return;
@@ -310,7 +322,7 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 #pragma unroll
   for (int j = 0; j < FB; ++j) {
     const int f = 4 * lane + 256 * j;
-    const float4 up = *reinterpret_cast<const float4*>(sV + wave * VP + f);
+    const float4 up = has_ad ? *reinterpret_cast<const float4*>(sV + wave * VP + f) : make_float4(0.f, 0.f, 0.f, 0.f);
     float zz[4];
     St<bf16>::ld4(sZ, wave * DP + f, zz);
     const float r4[4] = {__uint_as_float(rr[j].x << 16), __uint_as_float(rr[j].x & 0xffff0000u),
@@ -397,11 +409,14 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int NSTEP = SLICE / 32;
   constexpr bool PRE = FB <= 4;  // early loads while the registers allow
   constexpr int NPRE = PRE ? NSTEP : 1;
+  const bool has_ad = a.wup != nullptr;  // else: the norm backward only
   bf16x8 wup_f[NPRE];
   const bf16* wu = static_cast<const bf16*>(a.wup) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
   if constexpr (PRE) {
+    if (has_ad) {
 #pragma unroll
-    for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(wu + j * 32);
+      for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(wu + j * 32);
+    }
   }
 
   // ---- gradient at the adapter output (all loads issued up front)
@@ -453,6 +468,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     if (tv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), trow + f, dz[b]);
     St<bf16>::st4(sdZ, (long)l16 * DP + f, dz[b]);
   }
+  if (!has_ad) return;
   // W_down fragments of the last contraction, in flight during the dV one
   bf16x8 w0[FB], w1[FB];
   const bf16* wd = static_cast<const bf16*>(a.wdn) + (long)(f0 + l16) * MB + 8 * grp;
@@ -622,19 +638,22 @@ __global__ __launch_bounds__(256) void adapter_fwd_f32(AdapterFwdArgs a) {
   const float* res = static_cast<const float*>(a.res) + (long)t * d;
   const float* wdt = static_cast<const float*>(a.wdn_t);
   const float* wut = static_cast<const float*>(a.wup_t);
+  const bool has_ad = wdt != nullptr;  // else: residual add + norm only
   for (int i = threadIdx.x; i < d; i += blockDim.x) sz[i] = z[i];
   __syncthreads();
-  for (int j = threadIdx.x; j < m; j += blockDim.x) {
-    float u = 0.f;
-    for (int k = 0; k < d; ++k) u += sz[k] * wdt[(long)j * d + k];
-    if (a.u) static_cast<float*>(a.u)[(long)t * m + j] = u;
-    sg[j] = gelu_f(u);
-  }
+  if (has_ad)
+    for (int j = threadIdx.x; j < m; j += blockDim.x) {
+      float u = 0.f;
+      for (int k = 0; k < d; ++k) u += sz[k] * wdt[(long)j * d + k];
+      if (a.u) static_cast<float*>(a.u)[(long)t * m + j] = u;
+      sg[j] = gelu_f(u);
+    }
   __syncthreads();
   float s1 = 0.f;
   for (int f = threadIdx.x; f < d; f += blockDim.x) {
     float v = res[f] + sz[f];
-    for (int j = 0; j < m; ++j) v += sg[j] * wut[(long)f * m + j];
+    if (has_ad)
+      for (int j = 0; j < m; ++j) v += sg[j] * wut[(long)f * m + j];
     sv[f] = v;
     s1 += v;
   }
@@ -693,6 +712,7 @@ __global__ __launch_bounds__(256) void adapter_bwd_f32(AdapterBwdArgs a) {
     float* dzo = static_cast<float*>(a.dz) + (long)t * d;
     for (int f = threadIdx.x; f < d; f += blockDim.x) dzo[f] = sdz[f];
   }
+  if (!a.wup) return;  // no adapter: the norm backward (dz) is the whole result
   const float* wu = static_cast<const float*>(a.wup);
   const float* wd = static_cast<const float*>(a.wdn);
   const float* u = static_cast<const float*>(a.u) + (long)t * m;
@@ -793,15 +813,17 @@ static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s) {
-  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.z || !a.res || !a.wdn_t || !a.wup_t || !a.out)
+  // an absent adapter (both weight pointers NULL) leaves the residual add + norm
+  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.z || !a.res || !a.out || (!a.wdn_t != !a.wup_t))
     return hipErrorInvalidValue;
+  if (!a.wdn_t && a.u) return hipErrorInvalidValue;
   if (a.norm != Norm::None && !a.gamma) return hipErrorInvalidValue;
   if (a.norm == Norm::LN && !a.beta) return hipErrorInvalidValue;
   if (a.norm == Norm::RMS && !a.out_norm) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
   if (dtype == DT_BF16) {
     int nw, fb;
-    if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.z) || !al16(a.wdn_t) || !al16(a.wup_t))
+    if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.z) || (a.wdn_t && (!al16(a.wdn_t) || !al16(a.wup_t))))
       return hipErrorInvalidValue;
     switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
       case 1: return fwd_rows_k<1>(a, s);
@@ -821,15 +843,19 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
 }
 
 hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s) {
-  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.gin || !a.u || !a.wup || !a.wdn || !a.du)
-    return hipErrorInvalidValue;
+  // an absent adapter (both weight pointers NULL): only the norm backward, into dz
+  const bool has_ad = a.wup || a.wdn;
+  if (a.T < 0 || a.d <= 0 || a.m <= 0 || !a.gin) return hipErrorInvalidValue;
+  if (has_ad && (!a.u || !a.wup || !a.wdn || !a.du)) return hipErrorInvalidValue;
+  if (!has_ad && (!a.dz || a.dzin)) return hipErrorInvalidValue;
   if (!a.dz && a.norm != Norm::None) return hipErrorInvalidValue;
   if (a.norm != Norm::None && (!a.xhat || !a.rstd || !a.gamma)) return hipErrorInvalidValue;
   if (a.norm == Norm::RMS && !a.dres) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
   if (dtype == DT_BF16) {
     int nw, fb;
-    if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.wup) || !al16(a.wdn)) return hipErrorInvalidValue;
+    if (!bf16_shape(a.d, nw, fb) || a.m != MB || (has_ad && (!al16(a.wup) || !al16(a.wdn))))
+      return hipErrorInvalidValue;
     switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
       case 1: return bwd_k<16, 1>(a, s);
       case 2: return bwd_k<16, 2>(a, s);

@@ -134,6 +134,7 @@ hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* o
 template <typename T, bool UPDATE>
 __global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots, int d, int m, float lr) {
   const AdapterSlot sl = slots[blockIdx.y];
+  if (!sl.w_down) return;  // a block without this adapter (single placement)
   const long n = (long)d * m;
   for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < 2 * n; idx += (long)gridDim.x * blockDim.x) {
     if (idx < n) {

@@ -91,20 +91,31 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   L.blk.assign(D.n_blocks, BlockStash{});
   size_t cur = 0;
   auto take = [&](size_t n) { size_t o = cur; cur += n; return o; };
+  const bool single = D.placement == RINGADA_PLACEMENT_FFN;
   for (int l = 0; l < D.n_blocks; ++l) {
     BlockStash& b = L.blk[l];
     b = BlockStash{block_kind(l, c, D.n_blocks), NONE, NONE, NONE, NONE, NONE, NONE,
                    NONE, NONE, NONE, NONE, NONE, NONE};
     if (b.kind == K_NONE) continue;
     const bool full = b.kind == K_FULL;
+    if (single && !full) {
+      // the cut-off block stops after its FFN adapter: only that adapter's
+      // operands (and, post-LN, the LN2 backward that feeds it)
+      b.f2 = take(Td);
+      b.u2 = take(Tm);
+      if (!llama) { b.xhat2 = take(Td); b.rstd2 = take(rows); }
+      continue;
+    }
     if (full) {
       if (llama) { b.xhat1 = take(Td); b.rstd1 = take(rows); }
       b.qkv = take(T3d);
       b.o = take(Td);
       b.lse = take(lse);
     }
-    b.attn = take(Td);
-    b.u1 = take(Tm);
+    if (!single) {  // the attention adapter's operands
+      b.attn = take(Td);
+      b.u1 = take(Tm);
+    }
     if (!llama) { b.xhat1 = take(Td); b.rstd1 = take(rows); }
     if (llama) { b.xhat2 = take(Td); b.rstd2 = take(rows); }
     b.a1 = take(llama ? T2F : TF);
@@ -154,6 +165,8 @@ static ringada_status check_desc(const ringada_stage_desc* D) {
       D->max_batch < 1 || D->max_seq < 1)
     return fail(RINGADA_E_INVALID, "sizes must be positive");
   if (D->d_model % D->n_heads) return fail(RINGADA_E_INVALID, "d_model %% n_heads != 0");
+  if (D->placement != RINGADA_PLACEMENT_HOULSBY && D->placement != RINGADA_PLACEMENT_FFN)
+    return fail(RINGADA_E_INVALID, "unknown placement %d", D->placement);
   const int dh = D->d_model / D->n_heads;
   if (!(D->norm_eps >= 0.f)) return fail(RINGADA_E_INVALID, "norm_eps must be >= 0");
   if (D->arch == RINGADA_ARCH_PRERMS_SWIGLU && !(D->rope_theta > 0.f))
@@ -272,8 +285,12 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
                                                    const ringada_block_weights* w,
                                                    const ringada_adapter* attn, const ringada_adapter* ffn,
                                                    void* stream) {
-  if (!st || !w || !attn || !ffn) return fail(RINGADA_E_INVALID, "NULL argument");
+  if (!st || !w || !ffn) return fail(RINGADA_E_INVALID, "NULL argument");
   const ringada_stage_desc& D = st->D;
+  const bool single = D.placement == RINGADA_PLACEMENT_FFN;
+  if (single != (attn == nullptr))
+    return fail(RINGADA_E_INVALID, single ? "the single placement takes no attention adapter"
+                                          : "missing attention adapter");
   if (block < 0 || block >= D.n_blocks) return fail(RINGADA_E_INVALID, "block %d out of range", block);
   const bool post = D.arch == RINGADA_ARCH_POSTLN_GELU;
   if (!w->w_qkv || !w->w_o || !w->norm1_g || !w->w_in || !w->w_out || !w->norm2_g)
@@ -283,7 +300,8 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
   if (post && !has_post) return fail(RINGADA_E_INVALID, "post-LN block needs every bias and beta");
   if (!post && any_post) return fail(RINGADA_E_INVALID, "pre-RMS block takes no bias or beta");
   for (const ringada_adapter* a : {attn, ffn})
-    if (!a->w_down || !a->w_up || !a->g_down || !a->g_up) return fail(RINGADA_E_INVALID, "missing adapter tensor");
+    if (a && (!a->w_down || !a->w_up || !a->g_down || !a->g_up))
+      return fail(RINGADA_E_INVALID, "missing adapter tensor");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int dt = D.dtype;
   const size_t es = dt == RINGADA_BF16 ? 2 : 4;
@@ -294,12 +312,12 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
     RG_TRY(dalloc(st, d * d * es, &b.wt_o));
     RG_TRY(dalloc(st, (post ? 1 : 2) * F * d * es, &b.wt_in));
     RG_TRY(dalloc(st, d * F * es, &b.wt_out));
-    for (int a = 0; a < 2; ++a)
+    for (int a = single ? 1 : 0; a < 2; ++a)
       for (int k = 0; k < 4; ++k) RG_TRY(dalloc(st, d * m * es, &b.wk[a][k]));
   }
   if (!st->slots_dev) RG_TRY(dalloc(st, st->slots.size() * sizeof(AdapterSlot), (void**)&st->slots_dev));
   b.w = *w;
-  b.ad[0] = *attn;
+  b.ad[0] = attn ? *attn : ringada_adapter{};
   b.ad[1] = *ffn;
   RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), b.wt_qkv, s));
   RG_HIP(launch_transpose(dt, dt, w->w_o, (int)d, (int)d, b.wt_o, s));
@@ -434,14 +452,18 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
   const BlockBind& b = st->blocks[l];
   const Layout& L = st->L;
   const BlockStash& sb = L.blk[l];
-  const bool full = sb.kind == K_FULL, keep = sb.kind != K_NONE;
+  const bool single = st->D.placement == RINGADA_PLACEMENT_FFN;
   const int T = c.T, d = c.d, F = c.F, m = c.m;
   const double es = (double)c.es;
-  void* qkv = full ? c.S(sb.qkv) : c.W(L.qkv);
-  void* o = full ? c.S(sb.o) : c.W(L.o);
-  float* lse = static_cast<float*>(full ? c.S(sb.lse) : c.W(L.lse));
-  void* attn = keep ? c.S(sb.attn) : c.W(L.attn);
-  void* f2 = keep ? c.S(sb.f2) : c.W(L.f2);
+  // a tensor goes to its stash slot when the planner gave it one, else to
+  // the shared scratch (or nowhere, for the stash-only outputs)
+  auto SW = [&](size_t off, size_t scratch_off) { return off != NONE ? c.S(off) : c.W(scratch_off); };
+  auto SN = [&](size_t off) -> void* { return off != NONE ? c.S(off) : nullptr; };
+  void* qkv = SW(sb.qkv, L.qkv);
+  void* o = SW(sb.o, L.o);
+  float* lse = static_cast<float*>(SW(sb.lse, L.lse));
+  void* attn = SW(sb.attn, L.attn);
+  void* f2 = SW(sb.f2, L.f2);
   void* g = c.W(L.g);
   void* h1 = c.W(L.h1);
   const void* xin = X;
@@ -449,8 +471,8 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
   if (c.llama) {
     void* n1 = c.W(L.n1);
     RG_TRY(run(st, c.s, "rms_fwd", 0, es * 2.0 * T * d, [&] {
-      return launch_rms_fwd(c.dt, T, d, st->D.norm_eps, X, b.w.norm1_g, n1, full ? c.S(sb.xhat1) : nullptr,
-                            static_cast<float*>(full ? c.S(sb.rstd1) : nullptr), c.s);
+      return launch_rms_fwd(c.dt, T, d, st->D.norm_eps, X, b.w.norm1_g, n1, SN(sb.xhat1),
+                            static_cast<float*>(SN(sb.rstd1)), c.s);
     }));
     xin = n1;
   }
@@ -465,41 +487,43 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
 
   AdapterFwdArgs fa{};
   fa.T = T; fa.d = d; fa.m = m; fa.eps = st->D.norm_eps;
-  fa.z = attn; fa.res = X; fa.wdn_t = b.wk[0][1]; fa.wup_t = b.wk[0][3];
+  fa.z = attn; fa.res = X;
+  if (!single) { fa.wdn_t = b.wk[0][1]; fa.wup_t = b.wk[0][3]; }  // else residual add + norm only
   fa.gamma = c.llama ? b.w.norm2_g : b.w.norm1_g;
-  fa.u = keep ? c.S(sb.u1) : nullptr;
+  fa.u = SN(sb.u1);
   void* ffn_in;
   if (c.llama) {
     fa.norm = Norm::RMS; fa.out = h1; fa.out_norm = c.W(L.n2);
-    fa.xhat = keep ? c.S(sb.xhat2) : nullptr; fa.rstd = static_cast<float*>(keep ? c.S(sb.rstd2) : nullptr);
+    fa.xhat = SN(sb.xhat2); fa.rstd = static_cast<float*>(SN(sb.rstd2));
     ffn_in = c.W(L.n2);
   } else {
     fa.norm = Norm::LN; fa.beta = b.w.norm1_b; fa.out = h1;
-    fa.xhat = keep ? c.S(sb.xhat1) : nullptr; fa.rstd = static_cast<float*>(keep ? c.S(sb.rstd1) : nullptr);
+    fa.xhat = SN(sb.xhat1); fa.rstd = static_cast<float*>(SN(sb.rstd1));
     ffn_in = h1;
   }
   const double ad_flops = 4.0 * T * d * m;
-  RG_TRY(run(st, c.s, "adapter_fwd", ad_flops, es * (3.0 + (c.llama ? 1 : 0) + (keep ? 1 : 0)) * T * d,
+  RG_TRY(run(st, c.s, "adapter_fwd", single ? 0.0 : ad_flops,
+             es * (3.0 + (c.llama ? 1 : 0) + (fa.xhat ? 1 : 0)) * T * d,
              [&] { return launch_adapter_fwd(c.dt, fa, c.s); }));
   if (c.llama)
     RG_TRY(gemm(c, R_FFN_IN_FWD, Epi::SwiGlu, T, 2 * F, d, ffn_in, d, b.wt_in, d, g, F, nullptr, nullptr, 0,
-                keep ? c.S(sb.a1) : nullptr, 2 * F, F));
+                SN(sb.a1), 2 * F, F));
   else
     RG_TRY(gemm(c, R_FFN_IN_FWD, Epi::Gelu, T, F, d, ffn_in, d, b.wt_in, d, g, F, b.w.b_in, nullptr, 0,
-                keep ? c.S(sb.a1) : nullptr, F));
+                SN(sb.a1), F));
   RG_TRY(gemm(c, R_FFN_OUT_FWD, Epi::Store, T, d, F, g, F, b.wt_out, F, f2, d, b.w.b_out));
 
   AdapterFwdArgs fb{};
   fb.T = T; fb.d = d; fb.m = m; fb.eps = st->D.norm_eps;
   fb.z = f2; fb.res = h1; fb.wdn_t = b.wk[1][1]; fb.wup_t = b.wk[1][3];
-  fb.u = keep ? c.S(sb.u2) : nullptr; fb.out = Y;
+  fb.u = SN(sb.u2); fb.out = Y;
   if (c.llama) {
     fb.norm = Norm::None;
   } else {
     fb.norm = Norm::LN; fb.gamma = b.w.norm2_g; fb.beta = b.w.norm2_b;
-    fb.xhat = keep ? c.S(sb.xhat2) : nullptr; fb.rstd = static_cast<float*>(keep ? c.S(sb.rstd2) : nullptr);
+    fb.xhat = SN(sb.xhat2); fb.rstd = static_cast<float*>(SN(sb.rstd2));
   }
-  RG_TRY(run(st, c.s, "adapter_fwd", ad_flops, es * (3.0 + (keep && !c.llama ? 1 : 0)) * T * d,
+  RG_TRY(run(st, c.s, "adapter_fwd", ad_flops, es * (3.0 + (fb.xhat ? 1 : 0)) * T * d,
              [&] { return launch_adapter_fwd(c.dt, fb, c.s); }));
   return RINGADA_OK;
 }
@@ -570,11 +594,13 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   const double es = (double)c.es;
   void* du = c.W(L.du);
   const double ad_flops = 6.0 * T * d * m, dw_flops = 4.0 * T * d * m;
+  // under the single placement the block's lowest adapter is its FFN adapter
+  const bool single = st->D.placement == RINGADA_PLACEMENT_FFN, stop_ffn = single && stop;
 
   // FFN adapter (+ LN2 for post-LN)
   AdapterBwdArgs ab{};
   ab.T = T; ab.d = d; ab.m = m; ab.gin = G; ab.u = c.S(sb.u2);
-  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = du; ab.dzin = c.W(L.df2);
+  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = du; ab.dzin = stop_ffn ? nullptr : c.W(L.df2);
   const void* dz2;
   if (c.llama) {
     ab.norm = Norm::None; ab.dz = nullptr; dz2 = G;
@@ -582,10 +608,12 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
     ab.norm = Norm::LN; ab.xhat = c.S(sb.xhat2); ab.rstd = static_cast<const float*>(c.S(sb.rstd2));
     ab.gamma = b.w.norm2_g; ab.dz = c.W(L.dz2); dz2 = ab.dz;
   }
-  RG_TRY(run(st, c.s, "adapter_bwd", ad_flops, es * (c.llama ? 3.0 : 5.0) * T * d,
+  RG_TRY(run(st, c.s, "adapter_bwd", stop_ffn ? 4.0 * T * d * m : ad_flops,
+             es * ((c.llama ? 3.0 : 5.0) - (stop_ffn ? 1.0 : 0.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, ab, c.s); }));
   AdapterDwArgs dw{T, d, m, c.S(sb.u2), dz2, c.S(sb.f2), du, b.ad[1].g_up, b.ad[1].g_down};
   RG_TRY(run(st, c.s, "adapter_dw", dw_flops, es * 2.0 * T * d, [&] { return launch_adapter_dw(c.dt, dw, c.s); }));
+  if (stop_ffn) return RINGADA_OK;
 
   // FFN (dX only through frozen weights)
   void* da1 = c.W(L.da1);
@@ -598,11 +626,16 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
     RG_TRY(gemm(c, R_FFN_IN_DX, Epi::Resid, T, d, F, da1, F, b.w.w_in, F, c.W(L.dh1), d, nullptr, dz2, d));
   }
 
-  // attention adapter (+ LN1 / RMSNorm-2 backward)
+  // attention adapter (+ LN1 / RMSNorm-2 backward); without one (single
+  // placement) only the norm backward, whose output is then the gradient at
+  // the attention sublayer's output
   AdapterBwdArgs aa{};
-  aa.T = T; aa.d = d; aa.m = m; aa.gin = c.W(L.dh1); aa.u = c.S(sb.u1);
-  aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = du; aa.dz = c.W(L.dz1);
-  aa.dzin = stop ? nullptr : c.W(L.dattn);
+  aa.T = T; aa.d = d; aa.m = m; aa.gin = c.W(L.dh1); aa.dz = c.W(L.dz1);
+  if (!single) {
+    aa.u = c.S(sb.u1); aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = du;
+    aa.dzin = stop ? nullptr : c.W(L.dattn);
+  }
+  void* dattn = single ? c.W(L.dz1) : c.W(L.dattn);
   if (c.llama) {
     aa.norm = Norm::RMS; aa.dres = G; aa.xhat = c.S(sb.xhat2);
     aa.rstd = static_cast<const float*>(c.S(sb.rstd2)); aa.gamma = b.w.norm2_g;
@@ -610,15 +643,17 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
     aa.norm = Norm::LN; aa.xhat = c.S(sb.xhat1); aa.rstd = static_cast<const float*>(c.S(sb.rstd1));
     aa.gamma = b.w.norm1_g;
   }
-  RG_TRY(run(st, c.s, "adapter_bwd", stop ? 4.0 * T * d * m : ad_flops,
-             es * ((c.llama ? 4.0 : 3.0) + (stop ? 0.0 : 1.0)) * T * d,
+  RG_TRY(run(st, c.s, single ? "norm_bwd" : "adapter_bwd", single ? 0.0 : (stop ? 4.0 * T * d * m : ad_flops),
+             es * ((c.llama ? 4.0 : 3.0) + (stop || single ? 0.0 : 1.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, aa, c.s); }));
-  AdapterDwArgs dw1{T, d, m, c.S(sb.u1), c.W(L.dz1), c.S(sb.attn), du, b.ad[0].g_up, b.ad[0].g_down};
-  RG_TRY(run(st, c.s, "adapter_dw", dw_flops, es * 2.0 * T * d, [&] { return launch_adapter_dw(c.dt, dw1, c.s); }));
+  if (!single) {
+    AdapterDwArgs dw1{T, d, m, c.S(sb.u1), c.W(L.dz1), c.S(sb.attn), du, b.ad[0].g_up, b.ad[0].g_down};
+    RG_TRY(run(st, c.s, "adapter_dw", dw_flops, es * 2.0 * T * d, [&] { return launch_adapter_dw(c.dt, dw1, c.s); }));
+  }
   if (stop) return RINGADA_OK;
 
   // attention (dX only)
-  RG_TRY(gemm(c, R_O_DX, Epi::Store, T, d, d, c.W(L.dattn), d, b.w.w_o, d, c.W(L.dout), d));
+  RG_TRY(gemm(c, R_O_DX, Epi::Store, T, d, d, dattn, d, b.w.w_o, d, c.W(L.dout), d));
   AttnArgs at{};
   at.B = L.B; at.S = L.S; at.H = c.H; at.dh = c.dh;
   at.causal = c.llama; at.rope = c.llama; at.theta = st->D.rope_theta;

@@ -20,7 +20,8 @@ def make_desc(w: Workload, max_batch=None, max_seq=None):
         dtype=B.BF16 if w.dtype == "bf16" else B.F32,
         n_blocks=w.n_blocks, d_model=w.d_model, n_heads=w.n_heads, d_ffn=w.d_ffn,
         d_adapter=w.d_adapter, max_batch=max_batch or w.batch, max_seq=max_seq or w.seq,
-        norm_eps=1e-12 if w.arch == "bert" else 1e-6, rope_theta=10000.0)
+        norm_eps=1e-12 if w.arch == "bert" else 1e-6, rope_theta=10000.0,
+        placement=B.PLACEMENT_FFN if w.placement == "ffn" else B.PLACEMENT_HOULSBY)
 
 
 BERT_MAP = (("w_qkv", "w_qkv"), ("b_qkv", "b_qkv"), ("w_o", "w_o"), ("b_o", "b_o"),
@@ -58,7 +59,10 @@ class Stage:
             self.adapters.append(pair)
             bw = B.BlockWeights(**{k: v.data_ptr() for k, v in tens.items()})
             ca = [B.Adapter(**{k: v.data_ptr() for k, v in t.items()}) for t in pair]
-            B.ringada_stage_bind_block(self.handle, l, bw, ca[0], ca[1], self.sptr)
+            # the single placement binds no attention adapter (its tensors
+            # stay allocated here, untouched, so grads() keeps one layout)
+            B.ringada_stage_bind_block(self.handle, l, bw, None if w.placement == "ffn" else ca[0], ca[1],
+                                       self.sptr)
         self.stash = self.scratch = None
         self.stash_bytes = self.scratch_bytes = 0
 

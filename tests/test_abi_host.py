@@ -47,6 +47,19 @@ def test_stash_planner_bert_base_sweep():
     assert set(SWEEP) <= set(expect)
 
 
+def test_stash_planner_single_placement():
+    # one adapter per block, after the FFN (T = 4096, d = 768, bf16): a full
+    # block no longer keeps the attention adapter's input and down-projection
+    # (attn 6 MiB, u1 0.5 MiB): 66.72 MiB; the cut-off block stops after its
+    # FFN adapter and keeps only f2, u2 and LN2's xhat2, rstd2: 12.52 MiB
+    expect = {11: 12.52, 8: 3 * 66.72 + 12.52, -1: 12 * 66.72}
+    for c, mib in expect.items():
+        got, _ = plan_mib("bert_base_single", c)
+        assert abs(got - mib) < 0.05, (c, got, mib)
+    # the same scratch as the two-adapter stage
+    assert plan_mib("bert_base_single", 8)[1] == plan_mib("bert_base", 8)[1]
+
+
 def test_stash_planner_other_workloads():
     assert abs(plan_mib("llama7b_share", 6)[0] - 349.3) < 0.1
     assert abs(plan_mib("bert_large_share", 3)[0] - 259.6) < 0.1
@@ -95,6 +108,11 @@ def test_plan_and_create_validate_arguments():
     bad.n_heads = 7
     with pytest.raises(B.RingadaError) as e:
         B.ringada_stage_plan(bad, 1, 1, 0)
+    assert e.value.status == B.RINGADA_E_INVALID
+    bad = make_desc(w)
+    bad.placement = 2
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_create(bad)
     assert e.value.status == B.RINGADA_E_INVALID
     bad = make_desc(WORKLOADS["llama7b_share"])
     bad.dtype = B.F32

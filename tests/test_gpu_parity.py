@@ -8,7 +8,7 @@ import pytest
 from helpers import TOL, oracle_run, rel_err
 import oracle as O
 from paper_2502_19864_amd import binding as B
-from paper_2502_19864_amd.stage import Stage
+from paper_2502_19864_amd.stage import Stage, make_desc
 from paper_2502_19864_amd.workloads import SWEEP, WORKLOADS, Workload, make_inputs
 
 pytestmark = pytest.mark.gpu
@@ -33,6 +33,13 @@ SMALL = {
                                  "dy", 2003),
     "tiny_ragged": Workload("tiny_ragged", "bert", "f32", 2, 128, 2, 512, 16, 37, 3, 0, "dy", 2004,
                             tiny_adapter_init=True),
+    # the single serial adapter per block, after the FFN sublayer
+    "small_bert_single": Workload("small_bert_single", "bert", "bf16", 3, 256, 4, 512, 64, 100, 2, 1,
+                                  "dy", 2005, placement="ffn"),
+    "small_llama_single": Workload("small_llama_single", "llama", "bf16", 3, 256, 2, 384, 64, 100, 2, 1,
+                                   "dy", 2006, placement="ffn"),
+    "tiny_single": Workload("tiny_single", "bert", "f32", 3, 128, 2, 512, 16, 37, 3, 1, "dy", 2007,
+                            tiny_adapter_init=True, placement="ffn"),
 }
 
 
@@ -85,8 +92,8 @@ def check_grads(gpu, ref, lo, L, tol, tag):
         for a in range(2):
             for k in ("w_down", "w_up"):
                 g = gpu["grads"][l][a][k]
-                if l < lo:
-                    assert np.all(g == 0), (tag, "gradient below the cut-off", l, a, k)
+                if l < lo or ref["grads"][l][a] is None:  # frozen, or no such adapter
+                    assert np.all(g == 0), (tag, "gradient of a frozen or absent adapter", l, a, k)
                     continue
                 e = rel_err(g, ref["grads"][l][a][k])
                 worst = max(worst, e)
@@ -201,6 +208,27 @@ def test_bert_base_unfreezing_sweep(torch):
             gpu = run_gpu(torch, st, w, inp, c)
             assert rel_err(gpu["y"], ref["y"]) <= bound("y")
             check_grads(gpu, ref, c, w.n_blocks, bound, f"sweep c={c}")
+    finally:
+        st.close()
+
+
+def test_bert_base_single_placement_parity(torch):
+    """BERT-base-shaped stage with one adapter per block (after the FFN): the
+    backward ends after block 8's FFN adapter; the stash is the smaller plan."""
+    w = WORKLOADS["bert_base_single"]
+    inp = make_inputs(w)
+    st = Stage(w, inp)
+    try:
+        gpu = run_gpu(torch, st, w, inp, w.lowest_unfrozen)
+        ref = oracle_run(w, inp, w.lowest_unfrozen)
+        bound = floor_bounds(w, inp, w.lowest_unfrozen, ref)
+        print(f"[bert_base_single] y error {rel_err(gpu['y'], ref['y']):.3e}", flush=True)
+        assert rel_err(gpu["y"], ref["y"]) <= bound("y")
+        assert rel_err(gpu["g_wh"], ref["g_wh"]) <= bound("g_wh")
+        check_grads(gpu, ref, w.lowest_unfrozen, w.n_blocks, bound, "bert_base_single")
+        plan, _ = B.ringada_stage_plan(st.desc, w.batch, w.seq, w.lowest_unfrozen)
+        two, _ = B.ringada_stage_plan(make_desc(w.replace(placement="houlsby")), w.batch, w.seq, w.lowest_unfrozen)
+        assert plan < two
     finally:
         st.close()
 
