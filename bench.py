@@ -238,8 +238,9 @@ def main():
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": w.dtype, "data": "synthetic",
         "config": {"workload": f"{w.name}: {w.n_blocks} {'post-LN' if w.arch == 'bert' else 'pre-RMSNorm'} "
-                               f"blocks, d={w.d_model}, {w.n_heads} heads, FFN {w.d_ffn}, two adapters/block "
-                               f"m={w.d_adapter}, seq {w.seq}, batch {w.batch}, lowest unfrozen block {c}",
+                               f"blocks, d={w.d_model}, {w.n_heads} heads, FFN {w.d_ffn}, "
+                               + ("one adapter/block after the FFN" if w.placement == "ffn" else "two adapters/block")
+                               + f" m={w.d_adapter}, seq {w.seq}, batch {w.batch}, lowest unfrozen block {c}",
                    "batch": w.batch, "seq_len": w.seq, "n_blocks": w.n_blocks, "lowest_unfrozen": c,
                    "placement": w.placement,
                    "parallelism": "one ring stage on one GPU"},
