@@ -465,3 +465,44 @@ def local_lowest_unfrozen(n_tm, depth, beta, eps):
     if cut > eps:
         return eps - beta + 1
     return cut - beta
+
+
+# --------------------------------------------------------------------------
+# the top-down unfreezing schedule on one stage (Alg. 1)
+# --------------------------------------------------------------------------
+def depth_of_round(r, d0, k):
+    """Unfreezing depth in training round r (1-indexed): d0 in rounds 1..k,
+    then one more after every k rounds (the coordinator's d <- d + 1 once
+    r mod k == 0, Alg. 1)."""
+    return d0 + (r - 1) // k
+
+
+def alg1_stage_run(desc, weights, adapters, w_h, b_h, batches, n_tm, beta, d0, k,
+                   rounds, iters_per_round, lr, lr_head):
+    """Alg. 1's training loop for one initiator whose samples pass through
+    this stage (1-indexed Trm blocks beta .. beta + n_blocks - 1 of n_tm):
+    in round r the depth is depth_of_round(r, d0, k) and each of the
+    initiator's iterations runs the forward, the [CLS] loss, the head update
+    (with the head the forward used), the backward ending at the adapter the
+    depth selects, and the SGD update of the unfrozen adapters.  Iteration i
+    (0-based, over all rounds) takes batches[i % len(batches)] = (x, labels).
+    Returns (records, adapters, w_h, b_h), records[i] = (round, depth, c,
+    loss)."""
+    L = desc["n_blocks"]
+    eps_ = beta + L - 1
+    records = []
+    it = 0
+    for r in range(1, rounds + 1):
+        depth = min(depth_of_round(r, d0, k), n_tm)
+        c = local_lowest_unfrozen(n_tm, depth, beta, eps_)
+        for _ in range(iters_per_round):
+            x, labels = batches[it % len(batches)]
+            y, caches = stage_forward(desc, weights, adapters, x)
+            loss, dy, g_wh, g_bh = cls_head_ce(y, w_h, b_h, labels)
+            w_h, b_h = w_h - lr_head * g_wh, b_h - lr_head * g_bh
+            if c < L:
+                _, grads = stage_backward(desc, weights, adapters, caches, dy, c)
+                adapters = sgd_step(adapters, grads, lr)
+            records.append((r, depth, c, loss))
+            it += 1
+    return records, adapters, w_h, b_h
