@@ -1,5 +1,7 @@
 // Row-wise RMSNorm, parameter layout kernels, the adapter update and the
 // initiator's loss helpers.
+#include <algorithm>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -209,17 +211,18 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
 // sample: logits = y[b, 0, :] W_h + b_h, mean cross-entropy over the batch,
 // dy[b, 0, :] = dlogits W_h^T and zero at every other position, and the head
 // gradients accumulated into gwh / gbh.  Workgroup 0 does the head in two
-// phases per chunk of HEAD_CHUNK samples: (1) one wave per sample computes the
-// logits and dlogits into LDS, (2) one thread per feature i accumulates
-// gwh[i, :] over the chunk and writes dy[b, 0, i].  It alone owns gwh / gbh /
-// loss, so no atomics are needed.  The other workgroups zero the rows of dy
-// at positions 1..S-1.
+// phases per chunk of `chunk` samples: (1) one wave per sample computes the
+// logits and dlogits into LDS and copies the sample's [CLS] row into LDS,
+// (2) one thread per feature i accumulates gwh[i, :] over the chunk from
+// those LDS rows and writes dy[b, 0, i].  It alone owns gwh / gbh / loss, so
+// no atomics are needed.  The other workgroups zero the rows of dy at
+// positions 1..S-1.
 constexpr int HEAD_C = 16;      // maximum number of classes
 constexpr int HEAD_CHUNK = 64;  // samples per LDS chunk
 template <typename T>
 __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
                                                  const float* bh, int C, const int* labels, T* dy,
-                                                 float* gwh, float* gbh, float* loss) {
+                                                 float* gwh, float* gbh, float* loss, int chunk) {
   if (blockIdx.x > 0) {
     const int nz = gridDim.x - 1;
     for (int r = blockIdx.x - 1; r < B * S; r += nz) {
@@ -231,13 +234,15 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
   }
   __shared__ float sdl[HEAD_CHUNK][HEAD_C];
   __shared__ float sloss[HEAD_CHUNK];
+  extern __shared__ __attribute__((aligned(16))) unsigned char head_smem[];
+  T* sY = reinterpret_cast<T*>(head_smem);  // [chunk][d] rows of y at position 0
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   float total = 0.f;     // thread 0's running loss
   float gb[HEAD_C];      // thread 0's running bias gradient
 #pragma unroll
   for (int c = 0; c < HEAD_C; ++c) gb[c] = 0.f;
-  for (int b0 = 0; b0 < B; b0 += HEAD_CHUNK) {
-    const int nb = min(HEAD_CHUNK, B - b0);
+  for (int b0 = 0; b0 < B; b0 += chunk) {
+    const int nb = min(chunk, B - b0);
     // phase 1: logits and dlogits, one wave per sample
     for (int j = wave; j < nb; j += 4) {
       const T* row = y + (long)(b0 + j) * S * d;
@@ -245,7 +250,9 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
 #pragma unroll
       for (int c = 0; c < HEAD_C; ++c) lg[c] = 0.f;
       for (int i = lane; i < d; i += 64) {
-        const float yi = St<T>::ld(row, i);
+        const T raw = row[i];
+        sY[j * d + i] = raw;
+        const float yi = St<T>::ld(&raw, 0);
 #pragma unroll
         for (int c = 0; c < HEAD_C; ++c)
           if (c < C) lg[c] += yi * wh[(long)i * C + c];
@@ -283,7 +290,7 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
       }
       for (int j = 0; j < nb; ++j) {
         const long at = (long)(b0 + j) * S * d + i;
-        const float yi = St<T>::ld(y, at);
+        const float yi = St<T>::ld(sY, j * d + i);
         float g = 0.f;
 #pragma unroll
         for (int c = 0; c < HEAD_C; ++c)
@@ -321,12 +328,17 @@ hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const f
     return hipErrorInvalidValue;
   const long zero_rows = (long)B * (S - 1);
   const dim3 grid(1 + (unsigned)(zero_rows < 1024 ? zero_rows : 1024)), block(256);
+  // samples per chunk: their [CLS] rows staged in at most 64 KiB of LDS
+  const size_t es = dtype == DT_BF16 ? 2 : 4;
+  const int chunk = (int)std::min<long>(HEAD_CHUNK, (long)(65536 / (es * (size_t)d)));
+  if (chunk < 1) return hipErrorInvalidValue;
+  const size_t sh = (size_t)chunk * d * es;
   if (dtype == DT_BF16)
-    RG_LAUNCH(head_ce_k<bf16>, grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
-                       (bf16*)dy, gwh, gbh, loss);
+    RG_LAUNCH(head_ce_k<bf16>, grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
+                       (bf16*)dy, gwh, gbh, loss, chunk);
   else
-    RG_LAUNCH(head_ce_k<float>, grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels,
-                       (float*)dy, gwh, gbh, loss);
+    RG_LAUNCH(head_ce_k<float>, grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels,
+                       (float*)dy, gwh, gbh, loss, chunk);
   return hipGetLastError();
 }
 
