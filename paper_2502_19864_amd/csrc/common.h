@@ -147,6 +147,35 @@ __device__ __forceinline__ bf16x8 lds_tr_frag32(const bf16* tile, int pitch, int
   return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
 }
 
+// ---------------------------------------------------------------- packed adapter weights (bf16 path)
+// The bf16 adapter kernels run 16 waves over a d-wide row (d = 256 * FB) and
+// read the bottleneck weights only as MFMA 16x16x32 operand fragments.  The
+// working copies are stored in the order those fragments are read, so every
+// fragment load is one contiguous 1-KiB run (lane l at element 8 l):
+//  * layout A, for a [64][d] operand X (W_down^T in the forward, W_up in the
+//    backward): wave w = 4 ks + ug, k-step j < d / 128, lane = 16 grp + l16
+//    holds X[16 ug + l16][ks d/4 + 32 j + 8 grp + 0..7];
+//  * layout B, for a [d][64] operand X (W_up^T in the forward, W_down in the
+//    backward): wave w, block b < d / 256, half h, lane = 16 grp + l16 holds
+//    X[16 (FB w + b) + l16][32 h + 8 grp + 0..7].
+__host__ __device__ inline long pack_a_idx(int r, int c, int d) {  // X[r][c], r < 64, c < d
+  const int slice = d / 4, ks = c / slice, cc = c % slice, j = cc / 32, w8 = cc % 32;
+  const int wave = 4 * ks + r / 16, lane = 16 * (w8 / 8) + r % 16;
+  return ((long)(wave * (d / 128) + j) * 64 + lane) * 8 + w8 % 8;
+}
+__host__ __device__ inline long pack_b_idx(int r, int c, int d) {  // X[r][c], r < d, c < 64
+  const int fb = d / 256, wave = r / (16 * fb), rr = r % (16 * fb), b = rr / 16;
+  const int h = c / 32, cc = c % 32, lane = 16 * (cc / 8) + rr % 16;
+  return ((long)(wave * 2 * fb + 2 * b + h) * 64 + lane) * 8 + cc % 8;
+}
+// fragment (16 B) k-step j of wave w in layout A / block b, half h in layout B
+__device__ __forceinline__ const bf16* pack_a_frag(const void* base, int d, int wave, int j, int lane) {
+  return static_cast<const bf16*>(base) + ((long)(wave * (d / 128) + j) * 64 + lane) * 8;
+}
+__device__ __forceinline__ const bf16* pack_b_frag(const void* base, int d, int wave, int b, int h, int lane) {
+  return static_cast<const bf16*>(base) + ((long)(wave * 2 * (d / 256) + 2 * b + h) * 64 + lane) * 8;
+}
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

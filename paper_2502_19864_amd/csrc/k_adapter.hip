@@ -69,13 +69,12 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   // issued early while the registers allow (16-wave workgroups have 128 VGPRs)
   constexpr bool PRE = FB <= 4;
   bf16x8 w0[FB], w1[FB];
-  const bf16* wu = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
   if constexpr (PRE) {
     if (has_ad) {
 #pragma unroll
       for (int b = 0; b < FB; ++b) {
-        w0[b] = ld_frag(wu + (long)b * 16 * MB);
-        w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+        w0[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 0, lane));
+        w1[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 1, lane));
       }
     }
   }
@@ -84,7 +83,6 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:]
   if (has_ad) {
     const int ug = wave % 4, ks = wave / 4;
-    const bf16* wd = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
     const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
     f32x4 u = {0.f, 0.f, 0.f, 0.f};
     constexpr int NSTEP = SLICE / 32, RUN = NSTEP < 8 ? NSTEP : 8;
@@ -92,7 +90,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
     for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
       bf16x8 w[RUN];
 #pragma unroll
-      for (int j = 0; j < RUN; ++j) w[j] = ld_frag(wd + (k0 + j) * 32);
+      for (int j = 0; j < RUN; ++j) w[j] = ld_frag(pack_a_frag(a.wdn_t, D, wave, k0 + j, lane));
 #pragma unroll
       for (int j = 0; j < RUN; ++j) u = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), u);
     }
@@ -133,8 +131,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
       if (has_ad) {
 #pragma unroll
         for (int b = 0; b < FB; ++b) {
-          w0[b] = ld_frag(wu + (long)b * 16 * MB);
-          w1[b] = ld_frag(wu + (long)b * 16 * MB + 32);
+          w0[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 0, lane));
+          w1[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 1, lane));
         }
       }
     }
@@ -249,18 +247,16 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   const int ug = wave % 4, ks = wave / 4;
   bf16x8 wd[NSTEP];
   if (has_ad) {
-    const bf16* p = static_cast<const bf16*>(a.wdn_t) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
 #pragma unroll
-    for (int j = 0; j < NSTEP; ++j) wd[j] = ld_frag(p + j * 32);
+    for (int j = 0; j < NSTEP; ++j) wd[j] = ld_frag(pack_a_frag(a.wdn_t, D, wave, j, lane));
   }
   const int f0 = wave * 16 * FB;
   bf16x8 w0[FB], w1[FB];
   if (has_ad) {
-    const bf16* p = static_cast<const bf16*>(a.wup_t) + (long)(f0 + l16) * MB + 8 * grp;
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(p + (long)b * 16 * MB);
-      w1[b] = ld_frag(p + (long)b * 16 * MB + 32);
+      w0[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 0, lane));
+      w1[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 1, lane));
     }
   }
   const int tw = t0 + wave;  // this wave's token in the norm phase
@@ -411,11 +407,10 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int NPRE = PRE ? NSTEP : 1;
   const bool has_ad = a.wup != nullptr;  // else: the norm backward only
   bf16x8 wup_f[NPRE];
-  const bf16* wu = static_cast<const bf16*>(a.wup) + (long)(ug * 16 + l16) * D + ks * SLICE + 8 * grp;
   if constexpr (PRE) {
     if (has_ad) {
 #pragma unroll
-      for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(wu + j * 32);
+      for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
     }
   }
 
@@ -471,12 +466,11 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   if (!has_ad) return;
   // W_down fragments of the last contraction, in flight during the dV one
   bf16x8 w0[FB], w1[FB];
-  const bf16* wd = static_cast<const bf16*>(a.wdn) + (long)(f0 + l16) * MB + 8 * grp;
   if (PRE && a.dzin) {
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(wd + (long)b * 16 * MB);
-      w1[b] = ld_frag(wd + (long)b * 16 * MB + 32);
+      w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
+      w1[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 1, lane));
     }
   }
   __syncthreads();
@@ -497,7 +491,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
       for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
         bf16x8 w[RUN];
 #pragma unroll
-        for (int j = 0; j < RUN; ++j) w[j] = ld_frag(wu + (k0 + j) * 32);
+        for (int j = 0; j < RUN; ++j) w[j] = ld_frag(pack_a_frag(a.wup, D, wave, k0 + j, lane));
 #pragma unroll
         for (int j = 0; j < RUN; ++j) dv = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), dv);
       }
@@ -532,8 +526,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   if constexpr (!PRE) {
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(wd + (long)b * 16 * MB);
-      w1[b] = ld_frag(wd + (long)b * 16 * MB + 32);
+      w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
+      w1[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 1, lane));
     }
   }
 #pragma unroll

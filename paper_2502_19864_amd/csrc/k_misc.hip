@@ -1,6 +1,7 @@
 // Row-wise RMSNorm, parameter layout kernels, the adapter update and the
 // initiator's loss helpers.
 #include <algorithm>
+#include <type_traits>
 
 #include "common.h"
 #include "kernels.h"
@@ -147,8 +148,13 @@ __global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots
         sl.w_down[idx] = w;
         sl.g_down[idx] = 0.f;
       }
-      St<T>::st(static_cast<T*>(sl.wdn), idx, w);
-      St<T>::st(static_cast<T*>(sl.wdn_t), (long)j * d + i, w);
+      if constexpr (std::is_same_v<T, float>) {
+        St<T>::st(static_cast<T*>(sl.wdn), idx, w);
+        St<T>::st(static_cast<T*>(sl.wdn_t), (long)j * d + i, w);
+      } else {  // fragment-packed: W_down in layout B, W_down^T in layout A
+        St<T>::st(static_cast<T*>(sl.wdn), pack_b_idx(i, j, d), w);
+        St<T>::st(static_cast<T*>(sl.wdn_t), pack_a_idx(j, i, d), w);
+      }
     } else {
       const long k = idx - n;
       const int j = (int)(k / d), i = (int)(k % d);
@@ -158,8 +164,13 @@ __global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots
         sl.w_up[k] = w;
         sl.g_up[k] = 0.f;
       }
-      St<T>::st(static_cast<T*>(sl.wup), k, w);
-      St<T>::st(static_cast<T*>(sl.wup_t), (long)i * m + j, w);
+      if constexpr (std::is_same_v<T, float>) {
+        St<T>::st(static_cast<T*>(sl.wup), k, w);
+        St<T>::st(static_cast<T*>(sl.wup_t), (long)i * m + j, w);
+      } else {  // W_up in layout A, W_up^T in layout B
+        St<T>::st(static_cast<T*>(sl.wup), pack_a_idx(j, i, d), w);
+        St<T>::st(static_cast<T*>(sl.wup_t), pack_b_idx(i, j, d), w);
+      }
     }
   }
 }
