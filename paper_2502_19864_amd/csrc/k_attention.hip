@@ -28,20 +28,20 @@ __device__ __forceinline__ void rope_cs(int pos, int i, int dh, float log2theta,
 }
 
 // ================================================================ bf16 / MFMA
-constexpr int KT = 64;       // keys (or queries) per LDS tile
+constexpr int KT = 128;      // keys (or queries) per LDS tile: a whole 128-token sequence in one
 
 // Loads a [KT x DH] tile of rows r0.. (rows >= S are zero) from the Q/K/V
 // column block `col` into LDS row-major (pitch DH + 8), rotating pairs
 // (i, i + DH/2) when rot.
-template <int DH>
+template <int DH, int NT>
 __device__ __forceinline__ void load_tile(const bf16* qkv, int ld, int b, int S, int r0, int col,
                                           bool rot, float log2theta, bf16* rowmaj) {
   constexpr int HC = DH / 16;  // 8-element chunk pairs per row (chunk c with c + DH/16)
   constexpr int PAIRS = KT * HC;
-  static_assert(PAIRS % 256 == 0, "256-thread workgroups");
+  static_assert(PAIRS % NT == 0, "whole passes of the workgroup");
 #pragma unroll
-  for (int it = 0; it < PAIRS / 256; ++it) {
-    const int p = threadIdx.x + it * 256;
+  for (int it = 0; it < PAIRS / NT; ++it) {
+    const int p = threadIdx.x + it * NT;
     const int r = p / HC, c = p % HC, row = r0 + r;
     float x1[8], x2[8];
     if (row < S) {
@@ -145,13 +145,13 @@ __device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, 
     }
 }
 
-template <int DH, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
+template <int DH, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int q = blockIdx.x * 128 + wave * 32 + l32;
+  const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
   const float log2theta = a.rope ? log2f(a.theta) : 0.f;
@@ -169,16 +169,16 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float mrun = -INFINITY, lrun = 0.f;
 
-  const int qlast = min(S - 1, blockIdx.x * 128 + 127);
+  const int qlast = min(S - 1, blockIdx.x * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
+    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
+    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
     __syncthreads();
-    f32x16 sc[2];
+    f32x16 sc[KT / 32];
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KT / 32; ++kb) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) sc[kb][r] = 0.f;
 #pragma unroll
@@ -187,7 +187,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
     }
     float mx = -INFINITY;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KT / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kt * KT + kb * 32 + perm_pos(r, half);
@@ -200,7 +200,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
     const float alpha = exp2f(mrun - mnew);  // 0 on the first tile
     float rs = 0.f;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KT / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         sc[kb][r] = exp2f(sc[kb][r] - mnew);
@@ -214,7 +214,7 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
 #pragma unroll
       for (int r = 0; r < 16; ++r) oacc[i][r] *= alpha;
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
+    for (int kb = 0; kb < KT / 32; ++kb)
 #pragma unroll
       for (int j = 0; j < 2; ++j) {
         const bf16x8 pf = pack8(sc[kb], j);
@@ -231,13 +231,13 @@ __global__ __launch_bounds__(256) void attn_fwd_bf16(AttnArgs a) {
 }
 
 // dQ pass (lane = query); also writes D = rowsum(dO * O)
-template <int DH, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
+template <int DH, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_bwd_dq_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int q = blockIdx.x * 128 + wave * 32 + l32;
+  const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
   const float log2theta = a.rope ? log2f(a.theta) : 0.f;
@@ -273,15 +273,15 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-  const int qlast = min(S - 1, blockIdx.x * 128 + 127);
+  const int qlast = min(S - 1, blockIdx.x * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
-    load_tile<DH>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
+    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
+    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
     __syncthreads();
 #pragma unroll
-    for (int kb = 0; kb < 2; ++kb) {
+    for (int kb = 0; kb < KT / 32; ++kb) {
       f32x16 st, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) st[r] = dp[r] = 0.f;
@@ -313,14 +313,14 @@ __global__ __launch_bounds__(256) void attn_bwd_dq_bf16(AttnArgs a) {
 }
 
 // dK/dV pass (lane = key)
-template <int DH, bool CAUSAL>
-__global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
+template <int DH, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sQ[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
   __shared__ float sL[KT], sD[KT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
   const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int key = blockIdx.x * 128 + wave * 32 + l32;
+  const int key = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool kv = key < S;
   const int d = a.H * DH;
   const float log2theta = a.rope ? log2f(a.theta) : 0.f;
@@ -340,11 +340,11 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
     for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.f;
 
   const int nqt = (S + KT - 1) / KT;
-  const int qt0 = CAUSAL ? (blockIdx.x * 128) / KT : 0;
+  const int qt0 = CAUSAL ? (blockIdx.x * (32 * NW)) / KT : 0;
   for (int qt = qt0; qt < nqt; ++qt) {
     __syncthreads();
-    load_tile<DH>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ);
-    load_tile<DH>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO);
+    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ);
+    load_tile<DH, 64 * NW>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
       sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
@@ -352,7 +352,7 @@ __global__ __launch_bounds__(256) void attn_bwd_dkdv_bf16(AttnArgs a) {
     }
     __syncthreads();
 #pragma unroll
-    for (int qb = 0; qb < 2; ++qb) {
+    for (int qb = 0; qb < KT / 32; ++qb) {
       f32x16 st, dp;
 #pragma unroll
       for (int r = 0; r < 16; ++r) st[r] = dp[r] = 0.f;
@@ -521,22 +521,25 @@ __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
 // ================================================================ launchers
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 
+// four waves (128 queries or keys) per workgroup
+constexpr int ATT_NW = 4;
+
 template <int DH>
 static hipError_t fwd_dh(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
-  if (a.causal) RG_LAUNCH((attn_fwd_bf16<DH, true>), grid, block, 0, s, a);
-  else RG_LAUNCH((attn_fwd_bf16<DH, false>), grid, block, 0, s, a);
+  dim3 grid((a.S + 32 * ATT_NW - 1) / (32 * ATT_NW), a.B * a.H), block(64 * ATT_NW);
+  if (a.causal) RG_LAUNCH((attn_fwd_bf16<DH, true, ATT_NW>), grid, block, 0, s, a);
+  else RG_LAUNCH((attn_fwd_bf16<DH, false, ATT_NW>), grid, block, 0, s, a);
   return hipGetLastError();
 }
 template <int DH>
 static hipError_t bwd_dh(const AttnArgs& a, hipStream_t s) {
-  dim3 grid((a.S + 127) / 128, a.B * a.H), block(256);
+  dim3 grid((a.S + 32 * ATT_NW - 1) / (32 * ATT_NW), a.B * a.H), block(64 * ATT_NW);
   if (a.causal) {
-    RG_LAUNCH((attn_bwd_dq_bf16<DH, true>), grid, block, 0, s, a);
-    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, true>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dq_bf16<DH, true, ATT_NW>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, true, ATT_NW>), grid, block, 0, s, a);
   } else {
-    RG_LAUNCH((attn_bwd_dq_bf16<DH, false>), grid, block, 0, s, a);
-    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, false>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dq_bf16<DH, false, ATT_NW>), grid, block, 0, s, a);
+    RG_LAUNCH((attn_bwd_dkdv_bf16<DH, false, ATT_NW>), grid, block, 0, s, a);
   }
   return hipGetLastError();
 }
