@@ -221,64 +221,76 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
 // Initiator's classification head on the [CLS] (position 0) token of each
 // sample: logits = y[b, 0, :] W_h + b_h, mean cross-entropy over the batch,
 // dy[b, 0, :] = dlogits W_h^T and zero at every other position, and the head
-// gradients accumulated into gwh / gbh.  Workgroup 0 does the head in two
-// phases per chunk of `chunk` samples: (1) one wave per sample computes the
-// logits and dlogits into LDS and copies the sample's [CLS] row into LDS,
-// (2) one thread per feature i accumulates gwh[i, :] over the chunk from
-// those LDS rows and writes dy[b, 0, i].  It alone owns gwh / gbh / loss, so
-// no atomics are needed.  The other workgroups zero the rows of dy at
-// positions 1..S-1.
+// gradients accumulated into gwh / gbh.  Workgroup 0 does the head: W_h and,
+// per chunk of `chunk` samples, their [CLS] rows are copied to LDS with
+// 16-B loads (all in flight together); then (1) one wave per sample forms the
+// logits and dlogits, (2) one thread per feature i accumulates gwh[i, :] over
+// the chunk and writes dy[b, 0, i].  It alone owns gwh / gbh / loss, so no
+// atomics are needed.  The other workgroups zero dy at positions 1..S-1.
 constexpr int HEAD_C = 16;      // maximum number of classes
-constexpr int HEAD_CHUNK = 64;  // samples per LDS chunk
-template <typename T>
-__global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
+constexpr int HEAD_CHUNK = 64;  // maximum samples per LDS chunk
+constexpr int HEAD_NT = 1024;   // threads per workgroup (16 waves: the head does one sample per wave)
+template <typename T, int CN>  // CN: class count bound, compile time (the loops over classes unroll)
+__global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
                                                  const float* bh, int C, const int* labels, T* dy,
                                                  float* gwh, float* gbh, float* loss, int chunk) {
   if (blockIdx.x > 0) {
     const int nz = gridDim.x - 1;
+    const int vpr = d * (int)sizeof(T) / 16;  // 16-B vectors per row
     for (int r = blockIdx.x - 1; r < B * S; r += nz) {
       if (r % S == 0) continue;
-      T* row = dy + (long)r * d;
-      for (int i = threadIdx.x; i < d; i += 256) St<T>::st(row, i, 0.f);
+      uint4* row = reinterpret_cast<uint4*>(dy + (long)r * d);
+      for (int i = threadIdx.x; i < vpr; i += HEAD_NT) row[i] = make_uint4(0, 0, 0, 0);
     }
     return;
   }
-  __shared__ float sdl[HEAD_CHUNK][HEAD_C];
+  __shared__ float sdl[HEAD_CHUNK][CN];
   __shared__ float sloss[HEAD_CHUNK];
+  __shared__ float sbh[CN];
+  __shared__ int slab[HEAD_CHUNK];
   extern __shared__ __attribute__((aligned(16))) unsigned char head_smem[];
-  T* sY = reinterpret_cast<T*>(head_smem);  // [chunk][d] rows of y at position 0
+  float* sW = reinterpret_cast<float*>(head_smem);                              // [d][C]
+  T* sY = reinterpret_cast<T*>(head_smem + ((size_t)d * C * 4 + 15) / 16 * 16);  // [chunk][d]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  for (int i = threadIdx.x; i < d * C; i += HEAD_NT) sW[i] = wh[i];
+  if (threadIdx.x < C) sbh[threadIdx.x] = bh[threadIdx.x];
   float total = 0.f;     // thread 0's running loss
-  float gb[HEAD_C];      // thread 0's running bias gradient
+  float gb[CN];      // thread 0's running bias gradient
 #pragma unroll
-  for (int c = 0; c < HEAD_C; ++c) gb[c] = 0.f;
+  for (int c = 0; c < CN; ++c) gb[c] = 0.f;
+  const int vpr = d * (int)sizeof(T) / 16;
   for (int b0 = 0; b0 < B; b0 += chunk) {
     const int nb = min(chunk, B - b0);
+    // the chunk's [CLS] rows -> LDS, 16 B per load
+    if (threadIdx.x < nb) slab[threadIdx.x] = labels[b0 + threadIdx.x];
+#pragma unroll 4
+    for (int v = threadIdx.x; v < nb * vpr; v += HEAD_NT) {
+      const int j = v / vpr, k = v % vpr;
+      reinterpret_cast<uint4*>(sY + (long)j * d)[k] = reinterpret_cast<const uint4*>(y + (long)(b0 + j) * S * d)[k];
+    }
+    __syncthreads();
     // phase 1: logits and dlogits, one wave per sample
-    for (int j = wave; j < nb; j += 4) {
-      const T* row = y + (long)(b0 + j) * S * d;
-      float lg[HEAD_C];
+    for (int j = wave; j < nb; j += HEAD_NT / 64) {
+      float lg[CN];
 #pragma unroll
-      for (int c = 0; c < HEAD_C; ++c) lg[c] = 0.f;
+      for (int c = 0; c < CN; ++c) lg[c] = 0.f;
       for (int i = lane; i < d; i += 64) {
-        const T raw = row[i];
-        sY[j * d + i] = raw;
-        const float yi = St<T>::ld(&raw, 0);
+        const float yi = St<T>::ld(sY, (long)j * d + i);
 #pragma unroll
-        for (int c = 0; c < HEAD_C; ++c)
-          if (c < C) lg[c] += yi * wh[(long)i * C + c];
+        for (int c = 0; c < CN; ++c)
+          if (c < C) lg[c] += yi * sW[i * C + c];
       }
       float mx = -INFINITY;
 #pragma unroll
-      for (int c = 0; c < HEAD_C; ++c)
+      for (int c = 0; c < CN; ++c)
         if (c < C) {
-          lg[c] = wave_sum(lg[c]) + bh[c];
+          lg[c] = wave_sum(lg[c]) + sbh[c];
           mx = fmaxf(mx, lg[c]);
         }
       float se = 0.f, ll = 0.f;
-      const int lab = labels[b0 + j];
+      const int lab = slab[j];
 #pragma unroll
-      for (int c = 0; c < HEAD_C; ++c)
+      for (int c = 0; c < CN; ++c)
         if (c < C) {
           se += __expf(lg[c] - mx);
           if (c == lab) ll = lg[c];
@@ -286,47 +298,46 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
       if (lane == 0) {
         sloss[j] = -(ll - mx - __logf(se));
 #pragma unroll
-        for (int c = 0; c < HEAD_C; ++c)
+        for (int c = 0; c < CN; ++c)
           if (c < C) sdl[j][c] = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
       }
     }
     __syncthreads();
     // phase 2: one thread per feature
-    for (int i = threadIdx.x; i < d; i += 256) {
-      float w[HEAD_C], acc[HEAD_C];
+    for (int i = threadIdx.x; i < d; i += HEAD_NT) {
+      float w[CN], acc[CN];
 #pragma unroll
-      for (int c = 0; c < HEAD_C; ++c) {
-        w[c] = c < C ? wh[(long)i * C + c] : 0.f;
+      for (int c = 0; c < CN; ++c) {
+        w[c] = c < C ? sW[i * C + c] : 0.f;
         acc[c] = 0.f;
       }
       for (int j = 0; j < nb; ++j) {
-        const long at = (long)(b0 + j) * S * d + i;
-        const float yi = St<T>::ld(sY, j * d + i);
+        const float yi = St<T>::ld(sY, (long)j * d + i);
         float g = 0.f;
 #pragma unroll
-        for (int c = 0; c < HEAD_C; ++c)
+        for (int c = 0; c < CN; ++c)
           if (c < C) {
             acc[c] += yi * sdl[j][c];
             g += sdl[j][c] * w[c];
           }
-        St<T>::st(dy, at, g);
+        St<T>::st(dy, (long)(b0 + j) * S * d + i, g);
       }
 #pragma unroll
-      for (int c = 0; c < HEAD_C; ++c)
+      for (int c = 0; c < CN; ++c)
         if (c < C) gwh[(long)i * C + c] += acc[c];
     }
     if (threadIdx.x == 0)
       for (int j = 0; j < nb; ++j) {
         total += sloss[j];
 #pragma unroll
-        for (int c = 0; c < HEAD_C; ++c)
+        for (int c = 0; c < CN; ++c)
           if (c < C) gb[c] += sdl[j][c];
       }
     __syncthreads();
   }
   if (threadIdx.x == 0) {
 #pragma unroll
-    for (int c = 0; c < HEAD_C; ++c)
+    for (int c = 0; c < CN; ++c)
       if (c < C) gbh[c] += gb[c];
     if (loss) *loss = total / (float)B;
   }
@@ -337,19 +348,34 @@ hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const f
                           hipStream_t s) {
   if (!y || !wh || !bh || !labels || !dy || !gwh || !gbh || B <= 0 || S <= 0 || d <= 0 || C < 1 || C > HEAD_C)
     return hipErrorInvalidValue;
-  const long zero_rows = (long)B * (S - 1);
-  const dim3 grid(1 + (unsigned)(zero_rows < 1024 ? zero_rows : 1024)), block(256);
-  // samples per chunk: their [CLS] rows staged in at most 64 KiB of LDS
   const size_t es = dtype == DT_BF16 ? 2 : 4;
-  const int chunk = (int)std::min<long>(HEAD_CHUNK, (long)(65536 / (es * (size_t)d)));
-  if (chunk < 1) return hipErrorInvalidValue;
-  const size_t sh = (size_t)chunk * d * es;
-  if (dtype == DT_BF16)
-    RG_LAUNCH(head_ce_k<bf16>, grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
-                       (bf16*)dy, gwh, gbh, loss, chunk);
-  else
-    RG_LAUNCH(head_ce_k<float>, grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels,
-                       (float*)dy, gwh, gbh, loss, chunk);
+  // rows move as 16-B vectors: rows a multiple of 16 B, y and dy 16-B aligned
+  if ((d * es) % 16 || (reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(dy)) & 15u)
+    return hipErrorInvalidValue;
+  const long zero_rows = (long)B * (S - 1);
+  const dim3 grid(1 + (unsigned)(zero_rows < 256 ? zero_rows : 256)), block(HEAD_NT);
+  // LDS: W_h (d x C floats) and the chunk's rows, within 64 KiB together
+  // with the kernel's static arrays (dlogits, losses, labels of a chunk; bias)
+  const size_t budget = 65536 - sizeof(float) * (HEAD_CHUNK * (HEAD_C + 2) + HEAD_C);
+  const size_t wbytes = ((size_t)d * C * 4 + 15) / 16 * 16;
+  if (wbytes + es * d > budget) return hipErrorInvalidValue;
+  const int chunk = (int)std::min<size_t>(HEAD_CHUNK, (budget - wbytes) / (es * (size_t)d));
+  const size_t sh = wbytes + (size_t)chunk * d * es;
+  if (dtype == DT_BF16) {
+    if (C == 2)
+      RG_LAUNCH((head_ce_k<bf16, 2>), grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels, (bf16*)dy,
+                gwh, gbh, loss, chunk);
+    else
+      RG_LAUNCH((head_ce_k<bf16, HEAD_C>), grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
+                (bf16*)dy, gwh, gbh, loss, chunk);
+  } else {
+    if (C == 2)
+      RG_LAUNCH((head_ce_k<float, 2>), grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels, (float*)dy,
+                gwh, gbh, loss, chunk);
+    else
+      RG_LAUNCH((head_ce_k<float, HEAD_C>), grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels,
+                (float*)dy, gwh, gbh, loss, chunk);
+  }
   return hipGetLastError();
 }
 
