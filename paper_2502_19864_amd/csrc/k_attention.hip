@@ -232,7 +232,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
 
 // dQ pass (lane = query); also writes D = rowsum(dO * O)
 template <int DH, bool CAUSAL, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bwd_dq_bf16(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 64 ? 2 : 1))) void attn_bwd_dq_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
@@ -280,7 +280,9 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_bf16(AttnArgs a) {
     load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
     load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
     __syncthreads();
-#pragma unroll
+    // one key block at a time (not unrolled): keeps the kernel within the
+    // registers of two waves per SIMD, so a (batch, head) grid fits one round
+#pragma unroll 1
     for (int kb = 0; kb < KT / 32; ++kb) {
       f32x16 st, dp;
 #pragma unroll
@@ -314,7 +316,7 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dq_bf16(AttnArgs a) {
 
 // dK/dV pass (lane = key)
 template <int DH, bool CAUSAL, int NW>
-__global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_bf16(AttnArgs a) {
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 64 ? 2 : 1))) void attn_bwd_dkdv_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sQ[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
   __shared__ float sL[KT], sD[KT];
@@ -351,7 +353,8 @@ __global__ __launch_bounds__(64 * NW) void attn_bwd_dkdv_bf16(AttnArgs a) {
       sD[i] = qq < S ? a.dsum[(long)bh * S + qq] : 0.f;
     }
     __syncthreads();
-#pragma unroll
+    // one query block at a time (not unrolled), as in the dQ pass
+#pragma unroll 1
     for (int qb = 0; qb < KT / 32; ++qb) {
       f32x16 st, dp;
 #pragma unroll

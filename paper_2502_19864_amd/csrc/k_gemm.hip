@@ -337,7 +337,7 @@ constexpr int epi_rows(int bm, int row_bytes, int lds_bytes) {
 
 template <int BM, int BN, int WM, int WN, int BK, int NS, Epi E, int GROUP = 4>
 __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
-  constexpr int NW = WM * WN;
+  constexpr int NW = WM * WN, NT = 64 * NW;
   constexpr int TM = BM / WM, TN = BN / WN, FM = TM / 32, FN = TN / 32;
   constexpr int ROWB = BK * 2, CPR = BK / 8, RPI = 64 / CPR, SWD = 16 / CPR;
   constexpr int LA = BM / (RPI * NW), LB = BN / (RPI * NW), LPT = LA + LB;
@@ -497,9 +497,9 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
     if constexpr (E == Epi::SwiGlu) {
       // packed columns [64p, 64p+32) are gates, [64p+32, 64p+64) the matching ups
       constexpr int CPRW = BN / 16, NCH = RPP * CPRW;
-      static_assert(NCH % 256 == 0, "whole passes");
+      static_assert(NCH % NT == 0, "whole passes");
 #pragma unroll 2
-      for (int idx = tid; idx < NCH; idx += 256) {
+      for (int idx = tid; idx < NCH; idx += NT) {
         const int row = idx / CPRW, q = idx % CPRW, c = (q / 4) * 64 + (q % 4) * 8;
         const int m = m0 + p * RPP + row;
         if (m >= M || n0 + c >= N) continue;
@@ -510,9 +510,9 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
       }
     } else {
       constexpr int CPRW = BN / 8, NCH = RPP * CPRW;
-      static_assert(NCH % 256 == 0, "whole passes");
+      static_assert(NCH % NT == 0, "whole passes");
 #pragma unroll 2
-      for (int idx = tid; idx < NCH; idx += 256) {
+      for (int idx = tid; idx < NCH; idx += NT) {
         const int row = idx / CPRW, c = (idx % CPRW) * 8;
         const int m = m0 + p * RPP + row, n = n0 + c;
         if (m >= M || n >= N) continue;
@@ -620,8 +620,6 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
   if constexpr (!role_has(R, E)) {
     return hipErrorInvalidValue;
   } else {
-#define RG_NAME(SUFFIX)                                                                    \
-  (R == R_QKV_FWD ? 0 : 0)
     const dim3 block(256);
     if (dtype == DT_F32) {
       if constexpr (E == Epi::SwiGlu) return hipErrorInvalidValue;
@@ -677,7 +675,6 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
     }
 #undef RG_LAUNCH_CFG
 #undef RG_TILES
-#undef RG_NAME
     return hipGetLastError();
   }
 }
