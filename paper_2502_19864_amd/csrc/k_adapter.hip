@@ -113,7 +113,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
       if (a.u && tv) St<bf16>::st4(static_cast<bf16*>(a.u), (long)token * MB + ug * 16 + 4 * grp, uv);
       float gv[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) gv[r] = gelu_f(uv[r]);
+      for (int r = 0; r < 4; ++r) gv[r] = gelu_fast(uv[r]);
       St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
     }
   }
@@ -262,11 +262,15 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   const int tw = t0 + wave;  // this wave's token in the norm phase
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
-  uint2 rr[FB];
+  uint2 rr[FB], gmv[FB], btv[FB];
 #pragma unroll
-  for (int j = 0; j < FB; ++j)
-    rr[j] = twv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + 4 * lane + 256 * j)
-                : make_uint2(0, 0);
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    rr[j] = twv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + f) : make_uint2(0, 0);
+    // the norm's affine parameters, loaded with everything else rather than after the last barrier
+    gmv[j] = a.norm != Norm::None ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.gamma) + f) : make_uint2(0, 0);
+    btv[j] = a.norm == Norm::LN ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.beta) + f) : make_uint2(0, 0);
+  }
 #pragma unroll
   for (int i = 0; i < PER; ++i) {
     const int c = threadIdx.x + i * 1024, r = c / CPR, k = (c % CPR) * 8;
@@ -359,11 +363,13 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 #pragma unroll
   for (int j = 0; j < FB; ++j) {
     const int f = 4 * lane + 256 * j;
-    float xh[4], gm[4], bt[4] = {0.f, 0.f, 0.f, 0.f}, o[4];
+    float xh[4], o[4];
+    const float gm[4] = {__uint_as_float(gmv[j].x << 16), __uint_as_float(gmv[j].x & 0xffff0000u),
+                         __uint_as_float(gmv[j].y << 16), __uint_as_float(gmv[j].y & 0xffff0000u)};
+    const float bt[4] = {__uint_as_float(btv[j].x << 16), __uint_as_float(btv[j].x & 0xffff0000u),
+                         __uint_as_float(btv[j].y << 16), __uint_as_float(btv[j].y & 0xffff0000u)};
 #pragma unroll
     for (int q = 0; q < 4; ++q) xh[q] = (v[j][q] - mean) * rstd;
-    St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
-    if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
 #pragma unroll
     for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
     St<bf16>::st4(out, wrow + f, o);
@@ -413,6 +419,11 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
       for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
     }
   }
+
+  // pre-activation of this lane's four units (read in the dV phase), loaded now
+  const int ug0 = (wave % 4) * 16 + 4 * grp;
+  uint2 uraw = make_uint2(0, 0);
+  if (has_ad && tv && wave < 4) uraw = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.u) + (long)token * MB + ug0);
 
   // ---- gradient at the adapter output (all loads issued up front)
   float dz[FB][4];
@@ -479,8 +490,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   {
     const bf16* zr = sdZ + l16 * DP + ks * SLICE + 8 * grp;
     const int j0 = ug * 16 + 4 * grp;
-    float uu[4] = {0.f, 0.f, 0.f, 0.f};
-    if (tv && ks == 0) St<bf16>::ld4(static_cast<const bf16*>(a.u), (long)token * MB + j0, uu);
+    const float uu[4] = {__uint_as_float(uraw.x << 16), __uint_as_float(uraw.x & 0xffff0000u),
+                         __uint_as_float(uraw.y << 16), __uint_as_float(uraw.y & 0xffff0000u)};
     f32x4 dv = {0.f, 0.f, 0.f, 0.f};
     if constexpr (PRE) {
 #pragma unroll
@@ -513,7 +524,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     if (ks == 0) {
       float du[4];
 #pragma unroll
-      for (int r = 0; r < 4; ++r) du[r] = dv[r] * gelu_grad_f(uu[r]);
+      for (int r = 0; r < 4; ++r) du[r] = dv[r] * gelu_grad_fast(uu[r]);
       if (tv) St<bf16>::st4(static_cast<bf16*>(a.du), (long)token * MB + j0, du);
       St<bf16>::st4(sdU, (long)l16 * GP + j0, du);
     }
@@ -589,7 +600,7 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
         float f[8];
         unpack_frag(xv, f);
 #pragma unroll
-        for (int v = 0; v < 8; ++v) f[v] = gelu_f(f[v]);
+        for (int v = 0; v < 8; ++v) f[v] = gelu_fast(f[v]);
         xv = pack_frag(f);
       }
       *reinterpret_cast<bf16x8*>(sX + tt * GP + c * 8) = xv;
