@@ -30,40 +30,56 @@ __device__ __forceinline__ void rope_cs(int pos, int i, int dh, float log2theta,
 // ================================================================ bf16 / MFMA
 constexpr int KT = 128;      // keys (or queries) per LDS tile: a whole 128-token sequence in one
 
-// Loads a [KT x DH] tile of rows r0.. (rows >= S are zero) from the Q/K/V
-// column block `col` into LDS row-major (pitch DH + 8), rotating pairs
-// (i, i + DH/2) when rot.
+// Loads two [KT x DH] tiles of rows r0.. (rows >= S are zero), e.g. K and V,
+// from column blocks col0 / col1 into LDS row-major (pitch DH + 8), rotating
+// pairs (i, i + DH/2) of the first when rot0.  Every global load of both tiles
+// is issued before the first LDS store: the pair costs one memory round trip.
 template <int DH, int NT>
-__device__ __forceinline__ void load_tile(const bf16* qkv, int ld, int b, int S, int r0, int col,
-                                          bool rot, float log2theta, bf16* rowmaj) {
-  constexpr int HC = DH / 16;  // 8-element chunk pairs per row (chunk c with c + DH/16)
-  constexpr int PAIRS = KT * HC;
+__device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int col0, bool rot0, bf16* dst0,
+                                               const bf16* src1, int ld1, int col1, bf16* dst1, int b, int S,
+                                               int r0, float log2theta) {
+  constexpr int HC = DH / 16;
+  constexpr int PAIRS = KT * HC, IT = PAIRS / NT;
   static_assert(PAIRS % NT == 0, "whole passes of the workgroup");
+  bf16x8 raw[2][IT][2];
 #pragma unroll
-  for (int it = 0; it < PAIRS / NT; ++it) {
+  for (int it = 0; it < IT; ++it) {
     const int p = threadIdx.x + it * NT;
     const int r = p / HC, c = p % HC, row = r0 + r;
-    float x1[8], x2[8];
     if (row < S) {
-      const bf16* src = qkv + (long)(b * S + row) * ld + col;
-      unpack_frag(ld_frag(src + c * 8), x1);
-      unpack_frag(ld_frag(src + c * 8 + DH / 2), x2);
-      if (rot) {
-#pragma unroll
-        for (int v = 0; v < 8; ++v) {
-          float cs, sn;
-          rope_cs(row, c * 8 + v, DH, log2theta, &cs, &sn);
-          const float a = x1[v], bb = x2[v];
-          x1[v] = a * cs - bb * sn;
-          x2[v] = bb * cs + a * sn;
-        }
-      }
+      const bf16* a0 = src0 + (long)(b * S + row) * ld0 + col0 + c * 8;
+      const bf16* a1 = src1 + (long)(b * S + row) * ld1 + col1 + c * 8;
+      raw[0][it][0] = ld_frag(a0);
+      raw[0][it][1] = ld_frag(a0 + DH / 2);
+      raw[1][it][0] = ld_frag(a1);
+      raw[1][it][1] = ld_frag(a1 + DH / 2);
     } else {
-#pragma unroll
-      for (int v = 0; v < 8; ++v) x1[v] = x2[v] = 0.f;
+      raw[0][it][0] = raw[0][it][1] = raw[1][it][0] = raw[1][it][1] = zero_frag();
     }
-    *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8) = pack_frag(x1);
-    *reinterpret_cast<bf16x8*>(rowmaj + r * (DH + 8) + c * 8 + DH / 2) = pack_frag(x2);
+  }
+#pragma unroll
+  for (int it = 0; it < IT; ++it) {
+    const int p = threadIdx.x + it * NT;
+    const int r = p / HC, c = p % HC, row = r0 + r;
+    if (rot0 && row < S) {
+      float x1[8], x2[8];
+      unpack_frag(raw[0][it][0], x1);
+      unpack_frag(raw[0][it][1], x2);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) {
+        float cs, sn;
+        rope_cs(row, c * 8 + v, DH, log2theta, &cs, &sn);
+        const float a = x1[v], bb = x2[v];
+        x1[v] = a * cs - bb * sn;
+        x2[v] = bb * cs + a * sn;
+      }
+      raw[0][it][0] = pack_frag(x1);
+      raw[0][it][1] = pack_frag(x2);
+    }
+    *reinterpret_cast<bf16x8*>(dst0 + r * (DH + 8) + c * 8) = raw[0][it][0];
+    *reinterpret_cast<bf16x8*>(dst0 + r * (DH + 8) + c * 8 + DH / 2) = raw[0][it][1];
+    *reinterpret_cast<bf16x8*>(dst1 + r * (DH + 8) + c * 8) = raw[1][it][0];
+    *reinterpret_cast<bf16x8*>(dst1 + r * (DH + 8) + c * 8 + DH / 2) = raw[1][it][1];
   }
 }
 
@@ -173,8 +189,8 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
-    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
+                                kt * KT, log2theta);
     __syncthreads();
     f32x16 sc[KT / 32];
 #pragma unroll
@@ -185,25 +201,35 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
       for (int s = 0; s < DH / 16; ++s)
         sc[kb] = mfma32(ld_frag(sK + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), qf[s], sc[kb]);
     }
+    // the row max on the raw scores (the scale is positive), the scale folded
+    // into the exponent's FMA; masking only where a key can be out of range
+    // or in the future
     float mx = -INFINITY;
+    if (CAUSAL || (kt + 1) * KT > S) {
 #pragma unroll
-    for (int kb = 0; kb < KT / 32; ++kb)
+      for (int kb = 0; kb < KT / 32; ++kb)
 #pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int key = kt * KT + kb * 32 + perm_pos(r, half);
-        const bool ok = key < S && (!CAUSAL || key <= q);
-        sc[kb][r] = ok ? sc[kb][r] * sl2 : -INFINITY;
-        mx = fmaxf(mx, sc[kb][r]);
-      }
+        for (int r = 0; r < 16; ++r) {
+          const int key = kt * KT + kb * 32 + perm_pos(r, half);
+          const bool ok = key < S && (!CAUSAL || key <= q);
+          sc[kb][r] = ok ? sc[kb][r] : -INFINITY;
+          mx = fmaxf(mx, sc[kb][r]);
+        }
+    } else {
+#pragma unroll
+      for (int kb = 0; kb < KT / 32; ++kb)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) mx = fmaxf(mx, sc[kb][r]);
+    }
     mx = fmaxf(mx, __shfl_xor(mx, 32, 64));
-    const float mnew = fmaxf(mrun, mx);
-    const float alpha = exp2f(mrun - mnew);  // 0 on the first tile
+    const float mnew = fmaxf(mrun, mx * sl2);
+    const float alpha = __builtin_amdgcn_exp2f(mrun - mnew);  // 0 on the first tile
     float rs = 0.f;
 #pragma unroll
     for (int kb = 0; kb < KT / 32; ++kb)
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        sc[kb][r] = exp2f(sc[kb][r] - mnew);
+        sc[kb][r] = __builtin_amdgcn_exp2f(fmaf(sc[kb][r], sl2, -mnew));
         rs += sc[kb][r];
       }
     rs += __shfl_xor(rs, 32, 64);
@@ -276,9 +302,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const int qlast = min(S - 1, blockIdx.x * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
+    // every query of the workgroup and every key of the tile in range, no causal mask
+    const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
-    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, d + hd * DH, a.rope, log2theta, sK);
-    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, kt * KT, 2 * d + hd * DH, false, 0.f, sV);
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
+                                kt * KT, log2theta);
     __syncthreads();
     // one key block at a time (not unrolled): keeps the kernel within the
     // registers of two waves per SIMD, so a (batch, head) grid fits one round
@@ -295,8 +323,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int key = kt * KT + kb * 32 + perm_pos(r, half);
-        const bool ok = qv && key < S && (!CAUSAL || key <= q);
-        const float p = ok ? exp2f(st[r] * sl2 - lse) : 0.f;
+        const bool ok = full || (qv && key < S && (!CAUSAL || key <= q));
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(st[r], sl2, -lse)) : 0.f;
         st[r] = p * (dp[r] - dsum);  // dS
       }
 #pragma unroll
@@ -344,9 +372,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const int nqt = (S + KT - 1) / KT;
   const int qt0 = CAUSAL ? (blockIdx.x * (32 * NW)) / KT : 0;
   for (int qt = qt0; qt < nqt; ++qt) {
+    // every key of the workgroup and every query of the tile in range, no causal mask
+    const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
-    load_tile<DH, 64 * NW>(qkv, a.ld_qkv, b, S, qt * KT, hd * DH, a.rope, log2theta, sQ);
-    load_tile<DH, 64 * NW>(dO, a.ld_do, b, S, qt * KT, hd * DH, false, 0.f, sO);
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
+                                log2theta);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
       sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
@@ -368,8 +398,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
         const int qi = qb * 32 + perm_pos(r, half), qq = qt * KT + qi;
-        const bool ok = kv && qq < S && (!CAUSAL || key <= qq);
-        const float p = ok ? exp2f(st[r] * sl2 - sL[qi]) : 0.f;
+        const bool ok = full || (kv && qq < S && (!CAUSAL || key <= qq));
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(st[r], sl2, -sL[qi])) : 0.f;
         st[r] = p;
         ds[r] = p * (dp[r] - sD[qi]);
       }
