@@ -9,6 +9,8 @@
 // lanes sharing a token (shuffles) and then over waves (LDS).
 // Weight gradients are long-K (K = tokens), tiny-output contractions: a
 // split-K MFMA kernel with LDS-transposed tiles and fp32 atomics.
+#include <initializer_list>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -18,201 +20,11 @@ constexpr int TOK = 16;   // tokens per workgroup of the bf16 row kernels
 constexpr int MB = 64;    // adapter bottleneck of the bf16 path
 constexpr int GP = MB + 8;
 
-// ================================================================ bf16 forward
-// Workgroup: 16 tokens, NW waves, d = 16 * NW * FB features (wave w owns
-// features [w*16*FB, (w+1)*16*FB)).  Every global load is issued before the
-// first use: the z tile goes to LDS with coalesced 16-B loads, the residual is
-// prefetched into registers, weight fragments come from L2 in unrolled runs.
-template <int NW, int FB>
-__global__ __launch_bounds__(NW * 64) void adapter_fwd_bf16(AdapterFwdArgs a) {
-  constexpr int KS = NW / 4;           // k-splits of the down projection
-  constexpr int D = 16 * NW * FB, DP = D + 8;
-  constexpr int SLICE = D / KS;        // k range of one down-projection wave
-  static_assert(SLICE % 32 == 0, "k slice");
-  extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
-  bf16* sZ = reinterpret_cast<bf16*>(smem);                // [TOK][DP]
-  bf16* sG = sZ + TOK * DP;                                // [TOK][GP]
-  float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][TOK][MB]
-  float* sRed = sUp + KS * TOK * MB;                       // [NW][TOK]
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
-  const int T = a.T, t0 = blockIdx.x * TOK;
-  const int token = t0 + l16;
-  const bool tv = token < T;
-  const long trow = (long)(tv ? token : 0) * D;
-  const bf16* z = static_cast<const bf16*>(a.z);
-  const int f0 = wave * 16 * FB;
-  const bool has_ad = a.wdn_t != nullptr;  // else: residual add + norm only
-
-  // z tile -> LDS
-  {
-    constexpr int CPR = D / 8, NCH = TOK * CPR, PER = (NCH + NW * 64 - 1) / (NW * 64);
-    uint4 v[PER];
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * NW * 64, r = c / CPR, k = (c % CPR) * 8;
-      v[i] = (c < NCH && t0 + r < T) ? *reinterpret_cast<const uint4*>(z + (long)(t0 + r) * D + k)
-                                     : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < PER; ++i) {
-      const int c = threadIdx.x + i * NW * 64, r = c / CPR, k = (c % CPR) * 8;
-      if (c < NCH) *reinterpret_cast<uint4*>(sZ + r * DP + k) = v[i];
-    }
-  }
-  // residual (phase-2 layout: 4 consecutive features of one token, kept
-  // packed) and the up-projection fragments, all in flight with the z tile
-  uint2 rr[FB];
-#pragma unroll
-  for (int b = 0; b < FB; ++b)
-    rr[b] = tv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + trow + f0 + b * 16 + 4 * grp)
-               : make_uint2(0, 0);
-  // issued early while the registers allow (16-wave workgroups have 128 VGPRs)
-  constexpr bool PRE = FB <= 4;
-  bf16x8 w0[FB], w1[FB];
-  if constexpr (PRE) {
-    if (has_ad) {
-#pragma unroll
-      for (int b = 0; b < FB; ++b) {
-        w0[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 0, lane));
-        w1[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 1, lane));
-      }
-    }
-  }
-  __syncthreads();
-
-  // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:]
-  if (has_ad) {
-    const int ug = wave % 4, ks = wave / 4;
-    const bf16* zr = sZ + l16 * DP + ks * SLICE + 8 * grp;
-    f32x4 u = {0.f, 0.f, 0.f, 0.f};
-    constexpr int NSTEP = SLICE / 32, RUN = NSTEP < 8 ? NSTEP : 8;
-#pragma unroll
-    for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
-      bf16x8 w[RUN];
-#pragma unroll
-      for (int j = 0; j < RUN; ++j) w[j] = ld_frag(pack_a_frag(a.wdn_t, D, wave, k0 + j, lane));
-#pragma unroll
-      for (int j = 0; j < RUN; ++j) u = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), u);
-    }
-    if constexpr (KS > 1) {
-#pragma unroll
-      for (int r = 0; r < 4; ++r) sUp[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = u[r];
-      __syncthreads();
-      if (ks == 0) {
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float s = 0.f;
-#pragma unroll
-          for (int k2 = 0; k2 < KS; ++k2) s += sUp[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
-          u[r] = s;
-        }
-      }
-    }
-    if (ks == 0) {
-      float uv[4] = {u[0], u[1], u[2], u[3]};
-      if (a.u && tv) St<bf16>::st4(static_cast<bf16*>(a.u), (long)token * MB + ug * 16 + 4 * grp, uv);
-      float gv[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) gv[r] = gelu_fast(uv[r]);
-      St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
-    }
-  }
-  __syncthreads();
-
-  // ---- out^T[f][token] = W_up^T[f][:] . G[token][:]  + z + res
-  float v[FB][4];
-  {
-    bf16x8 g0 = zero_frag(), g1 = zero_frag();
-    if (has_ad) {
-      g0 = ld_frag(sG + l16 * GP + 8 * grp);
-      g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
-    }
-    if constexpr (!PRE) {
-      if (has_ad) {
-#pragma unroll
-        for (int b = 0; b < FB; ++b) {
-          w0[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 0, lane));
-          w1[b] = ld_frag(pack_b_frag(a.wup_t, D, wave, b, 1, lane));
-        }
-      }
-    }
-#pragma unroll
-    for (int b = 0; b < FB; ++b) {
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-      if (has_ad) {
-        acc = mfma16(w0[b], g0, acc);
-        acc = mfma16(w1[b], g1, acc);
-      }
-      float zz[4];
-      St<bf16>::ld4(sZ, l16 * DP + f0 + b * 16 + 4 * grp, zz);
-      const float r4[4] = {__uint_as_float(rr[b].x << 16), __uint_as_float(rr[b].x & 0xffff0000u),
-                           __uint_as_float(rr[b].y << 16), __uint_as_float(rr[b].y & 0xffff0000u)};
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[b][q] = acc[q] + zz[q] + r4[q];
-    }
-  }
-
-  auto row_sum = [&](float s) {  // sum over the token's features across the workgroup
-    s += __shfl_xor(s, 16, 64);
-    s += __shfl_xor(s, 32, 64);
-    if (grp == 0) sRed[wave * TOK + l16] = s;
-    __syncthreads();
-    float t = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) t += sRed[w * TOK + l16];
-    __syncthreads();
-    return t;
-  };
-
-  if (a.norm == Norm::None) {
-    if (tv)
-#pragma unroll
-      for (int b = 0; b < FB; ++b) St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
-    return;
-  }
-  constexpr float inv_d = 1.f / (float)D;
-  float mean = 0.f;
-  if (a.norm == Norm::LN) {
-    float s = 0.f;
-#pragma unroll
-    for (int b = 0; b < FB; ++b)
-#pragma unroll
-      for (int q = 0; q < 4; ++q) s += v[b][q];
-    mean = row_sum(s) * inv_d;
-  } else if (tv) {
-#pragma unroll
-    for (int b = 0; b < FB; ++b)  // RMS: the residual stream h itself is an output
-      St<bf16>::st4(static_cast<bf16*>(a.out), trow + f0 + b * 16 + 4 * grp, v[b]);
-  }
-  float s2 = 0.f;
-#pragma unroll
-  for (int b = 0; b < FB; ++b)
-#pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float c = v[b][q] - mean;
-      s2 += c * c;
-    }
-  const float rstd = rsqrtf(row_sum(s2) * inv_d + a.eps);
-  if (!tv) return;
-  if (a.rstd && wave == 0 && grp == 0) a.rstd[token] = rstd;
-  bf16* out = static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm);
-#pragma unroll
-  for (int b = 0; b < FB; ++b) {
-    const int f = f0 + b * 16 + 4 * grp;
-    float xh[4], gm[4], bt[4] = {0.f, 0.f, 0.f, 0.f}, o[4];
-#pragma unroll
-    for (int q = 0; q < 4; ++q) xh[q] = (v[b][q] - mean) * rstd;
-    St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm);
-    if (a.norm == Norm::LN) St<bf16>::ld4(static_cast<const bf16*>(a.beta), f, bt);
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
-    St<bf16>::st4(out, trow + f, o);
-    if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), trow + f, xh);
-  }
-}
-
-// Same computation for d <= 1024, laid out so that nothing waits twice on
-// memory and every global row access is contiguous: all global loads (the z
+// ================================================================ bf16 forward, d <= 1024
+// One workgroup of 16 waves per 16 tokens: the whole adapter, the residual
+// add and the norm in one kernel.
+// Laid out so that nothing waits twice on memory and every global row access
+// is contiguous: all global loads (the z
 // tile, the weight fragments of both projections, the residual) are issued
 // before the first barrier; the up projection's fp32 result is staged in LDS;
 // the add + norm phase then runs one wave per token (NW == TOK), so the row
@@ -620,6 +432,252 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
   }
 }
 
+// ================================================================ bf16, d > 1024
+// A 16-token workgroup holding the whole adapter would read all 2 x d x 64
+// weights (1 MB at d = 4096) for 16 tokens and leave half the GPU idle at
+// these token counts.  Wide widths split the work instead, in both directions:
+//   down:  P[kc][t][j] = sum over the features f of chunk kc (WIDE_KC features)
+//          of X[t][f] W[j][f], W in the A fragment layout (W_down^T forward,
+//          W_up backward); grid (T/16) x (d/WIDE_KC), no atomics;
+//   up:    S = sum_kc P (fp32), G = gelu(S) forward (S stashed as u) or
+//          G = S * gelu'(u) backward (G written as du); then, per chunk of
+//          WIDE_UC features, out = Z [+ R] + G W^T, W in the B fragment layout
+//          (W_up^T forward, W_down backward); grid (T/16) x (d/WIDE_UC);
+//   norm:  a row kernel for LayerNorm / RMSNorm forward or backward.
+// Both MFMA kernels use 16x16x32 with the weight as the A operand, as the row
+// kernels do, and read every operand fragment straight from global memory
+// (one contiguous 1-KB run per packed weight fragment).
+constexpr int WIDE_KC = 1024, WIDE_UC = 512;
+
+// packed-layout fragment of (unit group ug, 32-feature block fb) in layout A
+__device__ __forceinline__ const bf16* pack_a_block(const bf16* base, int d, int ug, int fb, int lane) {
+  const int per = d / 128;  // 32-feature blocks per quarter of the features
+  return base + ((long)((4 * (fb / per) + ug) * per + fb % per) * 64 + lane) * 8;
+}
+
+__global__ __launch_bounds__(256) void adapter_wide_down(const bf16* X, const bf16* Wa, int T, int d, float* P) {
+  __shared__ float red[4][MB][TOK + 1];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int t0 = blockIdx.x * TOK, kc = blockIdx.y;
+  const int token = t0 + l16;
+  const bool tv = token < T;
+  constexpr int NB = WIDE_KC / 4 / 32;  // 32-feature blocks per wave
+  const int fb0 = (kc * WIDE_KC + wave * (WIDE_KC / 4)) / 32;
+  const bf16* xr = X + (long)(tv ? token : 0) * d + fb0 * 32 + 8 * grp;
+  bf16x8 xf[NB];
+#pragma unroll
+  for (int j = 0; j < NB; ++j) xf[j] = tv ? ld_frag(xr + j * 32) : zero_frag();
+  f32x4 acc[4];
+#pragma unroll
+  for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    bf16x8 w[4];
+#pragma unroll
+    for (int g = 0; g < 4; ++g) w[g] = ld_frag(pack_a_block(Wa, d, g, fb0 + j, lane));
+#pragma unroll
+    for (int g = 0; g < 4; ++g) acc[g] = mfma16(w[g], xf[j], acc[g]);
+  }
+  // D[unit 16g + 4*grp + r][token l16]; the four waves' feature quarters summed in LDS
+#pragma unroll
+  for (int g = 0; g < 4; ++g)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) red[wave][16 * g + 4 * grp + r][l16] = acc[g][r];
+  __syncthreads();
+  for (int i = threadIdx.x; i < TOK * MB; i += 256) {
+    const int tok = i / MB, j = i % MB;
+    if (t0 + tok < T)
+      P[((long)kc * T + t0 + tok) * MB + j] = (red[0][j][tok] + red[1][j][tok]) + (red[2][j][tok] + red[3][j][tok]);
+  }
+}
+
+// BWD = false: G = gelu(S), S stashed in `uo` (may be null); BWD = true:
+// G = S * gelu'(ui), written to `uo`.  With Wb null only G is produced (the
+// backward at the cut-off, where no input gradient is wanted); then the grid
+// has one feature chunk.
+template <bool BWD>
+__global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, const bf16* ui, bf16* uo, int T,
+                                                       int d, const bf16* Wb, const bf16* Z, const bf16* R,
+                                                       bf16* out) {
+  __shared__ __attribute__((aligned(16))) bf16 sG[TOK * GP];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
+  const int t0 = blockIdx.x * TOK, fc = blockIdx.y;
+  for (int i = threadIdx.x; i < TOK * MB; i += 256) {
+    const int tok = i / MB, j = i % MB, t = t0 + tok;
+    float sum = 0.f, g = 0.f;
+    if (t < T) {
+      for (int kc = 0; kc < nkc; ++kc) sum += P[((long)kc * T + t) * MB + j];
+      if constexpr (BWD) {
+        g = sum * gelu_grad_fast(bf2f(ui[(long)t * MB + j]));
+        if (fc == 0) uo[(long)t * MB + j] = f2bf(g);
+      } else {
+        g = gelu_fast(sum);
+        if (fc == 0 && uo) uo[(long)t * MB + j] = f2bf(sum);
+      }
+    }
+    sG[tok * GP + j] = f2bf(g);
+  }
+  if (!Wb) return;
+  __syncthreads();
+  const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
+  const int token = t0 + l16;
+  const bool tv = token < T;
+  const long row = (long)(tv ? token : 0) * d;
+  constexpr int NBK = WIDE_UC / 16 / 4;  // 16-feature blocks per wave
+  const int b0 = (fc * WIDE_UC + wave * (WIDE_UC / 4)) / 16;
+  bf16x8 w[NBK][2];
+#pragma unroll
+  for (int b = 0; b < NBK; ++b) {
+    w[b][0] = ld_frag(Wb + ((long)(2 * (b0 + b)) * 64 + lane) * 8);
+    w[b][1] = ld_frag(Wb + ((long)(2 * (b0 + b) + 1) * 64 + lane) * 8);
+  }
+  uint2 zr[NBK], rr[NBK];
+#pragma unroll
+  for (int b = 0; b < NBK; ++b) {
+    const int f = (b0 + b) * 16 + 4 * grp;
+    zr[b] = tv ? *reinterpret_cast<const uint2*>(Z + row + f) : make_uint2(0, 0);
+    rr[b] = (tv && R) ? *reinterpret_cast<const uint2*>(R + row + f) : make_uint2(0, 0);
+  }
+#pragma unroll
+  for (int b = 0; b < NBK; ++b) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    acc = mfma16(w[b][0], g0, acc);
+    acc = mfma16(w[b][1], g1, acc);
+    if (!tv) continue;
+    float o[4];
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const uint32_t zw = q < 2 ? zr[b].x : zr[b].y, rw = q < 2 ? rr[b].x : rr[b].y;
+      const float zf = __uint_as_float((q & 1) ? (zw & 0xffff0000u) : (zw << 16));
+      const float rf = __uint_as_float((q & 1) ? (rw & 0xffff0000u) : (rw << 16));
+      o[q] = acc[q] + zf + rf;
+    }
+    St<bf16>::st4(out, row + (b0 + b) * 16 + 4 * grp, o);
+  }
+}
+
+// Row norms for wide widths: one 256-thread workgroup per token, eight
+// features per 16-B access (d <= 4096, so at most two per thread).
+constexpr int WIDE_NPT = 2;
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  const float t = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return t;
+}
+__device__ __forceinline__ void ld8f(const bf16* p, float v[8]) { unpack_frag(ld_frag(p), v); }
+__device__ __forceinline__ void st8f(bf16* p, const float v[8]) { *reinterpret_cast<bf16x8*>(p) = pack_frag(v); }
+
+// h = x1 (+ x2); LN: out = LN(h) g + b (out may alias x1); RMS: out = h (when
+// x2 is given) and out_norm = RMSNorm(h) g; None: out = h.  xhat, rstd stashed
+// when given.
+__global__ __launch_bounds__(256) void adapter_wide_norm_fwd(int d, float eps, Norm norm, const bf16* x1,
+                                                             const bf16* x2, const bf16* gamma, const bf16* beta,
+                                                             bf16* out, bf16* out_norm, bf16* xhat, float* rstd) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  const int nc = d / 8;
+  float v[WIDE_NPT][8];
+#pragma unroll
+  for (int i = 0; i < WIDE_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    ld8f(x1 + row + 8 * c, v[i]);
+    if (x2) {
+      float y[8];
+      ld8f(x2 + row + 8 * c, y);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[i][q] += y[q];
+    }
+  }
+  if (norm == Norm::None || (norm == Norm::RMS && x2)) {
+#pragma unroll
+    for (int i = 0; i < WIDE_NPT; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      if (c < nc) st8f(out + row + 8 * c, v[i]);
+    }
+    if (norm == Norm::None) return;
+  }
+  float mean = 0.f;
+  if (norm == Norm::LN) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < WIDE_NPT; ++i)
+      if (threadIdx.x + 256 * i < nc)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s += v[i][q];
+    mean = block_sum256(s, red) / (float)d;
+  }
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < WIDE_NPT; ++i)
+    if (threadIdx.x + 256 * i < nc)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float c = v[i][q] - mean;
+        s2 += c * c;
+      }
+  const float rs = rsqrtf(block_sum256(s2, red) / (float)d + eps);
+  if (rstd && threadIdx.x == 0) rstd[blockIdx.x] = rs;
+  bf16* dst = norm == Norm::LN ? out : out_norm;
+#pragma unroll
+  for (int i = 0; i < WIDE_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float xh[8], g[8], b[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
+    ld8f(gamma + 8 * c, g);
+    if (norm == Norm::LN) ld8f(beta + 8 * c, b);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      xh[q] = (v[i][q] - mean) * rs;
+      o[q] = xh[q] * g[q] + b[q];
+    }
+    st8f(dst + row + 8 * c, o);
+    if (xhat) st8f(xhat + row + 8 * c, xh);
+  }
+}
+
+// dz = [dres +] rstd (g*gin - [mean(g*gin)] - xhat mean(g*gin*xhat)), LN or RMS
+__global__ __launch_bounds__(256) void adapter_wide_norm_bwd(int d, Norm norm, const bf16* gin, const bf16* xhat,
+                                                             const float* rstd, const bf16* gamma,
+                                                             const bf16* dres, bf16* dz) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  const int nc = d / 8;
+  float gg[WIDE_NPT][8], xh[WIDE_NPT][8];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < WIDE_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float g[8];
+    ld8f(gin + row + 8 * c, gg[i]);
+    ld8f(xhat + row + 8 * c, xh[i]);
+    ld8f(gamma + 8 * c, g);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      gg[i][q] *= g[q];
+      s1 += gg[i][q];
+      s2 += gg[i][q] * xh[i][q];
+    }
+  }
+  const float m1 = norm == Norm::LN ? block_sum256(s1, red) / (float)d : 0.f;
+  const float m2 = block_sum256(s2, red) / (float)d, rs = rstd[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < WIDE_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float r[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
+    if (norm == Norm::RMS) ld8f(dres + row + 8 * c, r);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o[q] = r[q] + rs * (gg[i][q] - m1 - xh[i][q] * m2);
+    st8f(dz + row + 8 * c, o);
+  }
+}
+
 // ================================================================ fp32 (small stages): one workgroup per token
 __device__ float block_sum(float v, float* red) {
   v = wave_sum(v);
@@ -787,21 +845,6 @@ static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
 }
 
 template <int NW, int FB>
-static hipError_t fwd_k(const AdapterFwdArgs& a, hipStream_t s) {
-  constexpr int D = 16 * NW * FB;
-  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
-                    (size_t)NW * TOK * 4;
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_fwd_bf16<NW, FB>),
-                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)sh);
-    if (e != hipSuccess) return e;
-    attr = true;
-  }
-  RG_LAUNCH((adapter_fwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
-  return hipGetLastError();
-}
-template <int NW, int FB>
 static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
   constexpr int D = 16 * NW * FB;
   const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
@@ -814,6 +857,59 @@ static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
     attr = true;
   }
   RG_LAUNCH((adapter_bwd_bf16<NW, FB>), dim3((a.T + TOK - 1) / TOK), dim3(NW * 64), sh, s, a);
+  return hipGetLastError();
+}
+
+long adapter_part_elems(int dtype, int T, int d, int m) {
+  return (dtype == DT_BF16 && d > 1024) ? (long)(d / WIDE_KC) * T * m : 0;
+}
+
+static hipError_t fwd_wide(const AdapterFwdArgs& a, hipStream_t s) {
+  if (a.d % WIDE_KC || a.d / 8 > 256 * WIDE_NPT || (a.wdn_t && !a.part)) return hipErrorInvalidValue;
+  for (const void* p : std::initializer_list<const void*>{a.z, a.res, a.out, a.out_norm, a.xhat, a.gamma, a.beta})  // 16-B row accesses
+    if (p && !al16(p)) return hipErrorInvalidValue;
+  const bf16* z = static_cast<const bf16*>(a.z);
+  const bf16* res = static_cast<const bf16*>(a.res);
+  const int ntok = (a.T + TOK - 1) / TOK, nkc = a.d / WIDE_KC, nuc = a.d / WIDE_UC;
+  bf16* out = static_cast<bf16*>(a.out);
+  if (a.wdn_t) {
+    RG_LAUNCH(adapter_wide_down, dim3(ntok, nkc), dim3(256), 0, s, z, static_cast<const bf16*>(a.wdn_t), a.T,
+              a.d, a.part);
+    RG_LAUNCH((adapter_wide_up<false>), dim3(ntok, nuc), dim3(256), 0, s, a.part, nkc, nullptr,
+              static_cast<bf16*>(a.u), a.T, a.d, static_cast<const bf16*>(a.wup_t), z, res, out);
+    if (a.norm != Norm::None)  // the norm of h, now in out
+      RG_LAUNCH(adapter_wide_norm_fwd, dim3(a.T), dim3(256), 0, s, a.d, a.eps, a.norm, out, nullptr,
+                static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.beta), out,
+                static_cast<bf16*>(a.out_norm), static_cast<bf16*>(a.xhat), a.rstd);
+  } else {
+    RG_LAUNCH(adapter_wide_norm_fwd, dim3(a.T), dim3(256), 0, s, a.d, a.eps, a.norm, z, res,
+              static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.beta), out,
+              static_cast<bf16*>(a.out_norm), static_cast<bf16*>(a.xhat), a.rstd);
+  }
+  return hipGetLastError();
+}
+
+static hipError_t bwd_wide(const AdapterBwdArgs& a, hipStream_t s) {
+  const bool has_ad = a.wup != nullptr;
+  if (a.d % WIDE_KC || a.d / 8 > 256 * WIDE_NPT || (has_ad && !a.part)) return hipErrorInvalidValue;
+  for (const void* p : std::initializer_list<const void*>{a.gin, a.dres, a.xhat, a.gamma, a.dz, a.dzin})  // 16-B row accesses
+    if (p && !al16(p)) return hipErrorInvalidValue;
+  const bf16* dZ = static_cast<const bf16*>(a.gin);
+  if (a.norm != Norm::None) {
+    RG_LAUNCH(adapter_wide_norm_bwd, dim3(a.T), dim3(256), 0, s, a.d, a.norm, dZ, static_cast<const bf16*>(a.xhat),
+              a.rstd, static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.dres), static_cast<bf16*>(a.dz));
+    dZ = static_cast<const bf16*>(a.dz);
+  } else if (a.dz && a.dz != a.gin) {  // no norm: the adapter-output gradient is gin itself
+    const hipError_t e = hipMemcpyAsync(a.dz, a.gin, (size_t)a.T * a.d * 2, hipMemcpyDeviceToDevice, s);
+    if (e != hipSuccess) return e;
+  }
+  if (!has_ad) return hipGetLastError();
+  const int ntok = (a.T + TOK - 1) / TOK, nkc = a.d / WIDE_KC, nuc = a.d / WIDE_UC;
+  RG_LAUNCH(adapter_wide_down, dim3(ntok, nkc), dim3(256), 0, s, dZ, static_cast<const bf16*>(a.wup), a.T, a.d,
+            a.part);
+  RG_LAUNCH((adapter_wide_up<true>), dim3(ntok, a.dzin ? nuc : 1), dim3(256), 0, s, a.part, nkc,
+            static_cast<const bf16*>(a.u), static_cast<bf16*>(a.du), a.T, a.d,
+            a.dzin ? static_cast<const bf16*>(a.wdn) : nullptr, dZ, nullptr, static_cast<bf16*>(a.dzin));
   return hipGetLastError();
 }
 
@@ -835,9 +931,7 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
       case 2: return fwd_rows_k<2>(a, s);
       case 3: return fwd_rows_k<3>(a, s);
       case 4: return fwd_rows_k<4>(a, s);
-      case 8: return fwd_k<16, 8>(a, s);
-      case 12: return fwd_k<16, 12>(a, s);
-      case 16: return fwd_k<16, 16>(a, s);
+      default: return fwd_wide(a, s);  // d = 2048, 3072, 4096
     }
     return hipErrorInvalidValue;
   }
@@ -866,9 +960,7 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
       case 2: return bwd_k<16, 2>(a, s);
       case 3: return bwd_k<16, 3>(a, s);
       case 4: return bwd_k<16, 4>(a, s);
-      case 8: return bwd_k<16, 8>(a, s);
-      case 12: return bwd_k<16, 12>(a, s);
-      case 16: return bwd_k<16, 16>(a, s);
+      default: return bwd_wide(a, s);  // d = 2048, 3072, 4096
     }
     return hipErrorInvalidValue;
   }

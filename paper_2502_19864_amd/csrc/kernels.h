@@ -98,6 +98,8 @@ struct AdapterFwdArgs {
   void* u;            // stash of z W_down [T, m] (may be null)
   void* xhat;         // stash of the normalised input [T, d] (may be null)
   float* rstd;        // stash [T] (may be null)
+  float* part;        // bf16 with d > 1024: fp32 scratch [d / 1024][T][m] for the
+                      // split-K partial sums of z W_down; unused otherwise
 };
 hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s);
 
@@ -118,7 +120,11 @@ struct AdapterBwdArgs {
                       // Norm::None (it equals gin)
   void* du;           // gradient at z W_down [T, m] (always written)
   void* dzin;         // gradient at the adapter input [T, d]; null = skip
+  float* part;        // bf16 with d > 1024: fp32 scratch [d / 1024][T][m] for the
+                      // split-K partial sums of dZ W_up^T; unused otherwise
 };
+// fp32 elements of the scratch `part` needs (0 when the shape takes none)
+long adapter_part_elems(int dtype, int T, int d, int m);
 hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s);
 
 // dW_up[m, d] += gelu(U)^T dZ ; dW_down[d, m] += Z^T dU   (fp32 accumulators)

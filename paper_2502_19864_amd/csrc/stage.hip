@@ -65,6 +65,7 @@ struct Layout {
   size_t act[2], h1, n1, n2, qkv, o, lse, attn, g, f2;
   // backward scratch (aliases the forward scratch: dead after the forward)
   size_t dact[2], dz2, df2, da1, dh1, dz1, dattn, dout, dqkv, du, dsum, dn1;
+  size_t adp;  // both passes
 };
 
 static size_t al256(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -152,7 +153,12 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   L.du = take(Tm);
   L.dsum = take(lse);
   L.dn1 = llama ? take(Td) : NONE;
-  L.scratch_bytes = std::max(fwd, cur);
+  // split-K partials of the wide (d > 1024) adapter kernels, used inside one
+  // adapter call in either pass: after both lists
+  const long part = adapter_part_elems(D.dtype, (int)T, (int)d, (int)m);
+  cur = std::max(fwd, cur);
+  L.adp = part > 0 ? take(al256((size_t)part * 4)) : NONE;
+  L.scratch_bytes = cur;
 }
 
 static ringada_status check_desc(const ringada_stage_desc* D) {
@@ -490,7 +496,7 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
   fa.z = attn; fa.res = X;
   if (!single) { fa.wdn_t = b.wk[0][1]; fa.wup_t = b.wk[0][3]; }  // else residual add + norm only
   fa.gamma = c.llama ? b.w.norm2_g : b.w.norm1_g;
-  fa.u = SN(sb.u1);
+  fa.u = SN(sb.u1); fa.part = static_cast<float*>(c.W(L.adp));
   void* ffn_in;
   if (c.llama) {
     fa.norm = Norm::RMS; fa.out = h1; fa.out_norm = c.W(L.n2);
@@ -516,7 +522,7 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
   AdapterFwdArgs fb{};
   fb.T = T; fb.d = d; fb.m = m; fb.eps = st->D.norm_eps;
   fb.z = f2; fb.res = h1; fb.wdn_t = b.wk[1][1]; fb.wup_t = b.wk[1][3];
-  fb.u = SN(sb.u2); fb.out = Y;
+  fb.u = SN(sb.u2); fb.out = Y; fb.part = static_cast<float*>(c.W(L.adp));
   if (c.llama) {
     fb.norm = Norm::None;
   } else {
@@ -601,6 +607,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   AdapterBwdArgs ab{};
   ab.T = T; ab.d = d; ab.m = m; ab.gin = G; ab.u = c.S(sb.u2);
   ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = du; ab.dzin = stop_ffn ? nullptr : c.W(L.df2);
+  ab.part = static_cast<float*>(c.W(L.adp));
   const void* dz2;
   if (c.llama) {
     ab.norm = Norm::None; ab.dz = nullptr; dz2 = G;
@@ -631,6 +638,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   // the attention sublayer's output
   AdapterBwdArgs aa{};
   aa.T = T; aa.d = d; aa.m = m; aa.gin = c.W(L.dh1); aa.dz = c.W(L.dz1);
+  aa.part = static_cast<float*>(c.W(L.adp));
   if (!single) {
     aa.u = c.S(sb.u1); aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = du;
     aa.dzin = stop ? nullptr : c.W(L.dattn);

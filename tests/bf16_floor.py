@@ -118,7 +118,9 @@ def bert_floor(w, inp, c, ref):
         dy = _rb(dy)
     else:
         dy = np.asarray(inp["dy"], np.float64)
-    _, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
+    dx_emu, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
+    if c < 0 and ref.get("dx") is not None:
+        out["dx"] = rel_err(dx_emu, ref["dx"])
     for l in range(max(c, 0), w.n_blocks):
         for a in range(2):
             if g_emu[l][a] is None:
@@ -137,21 +139,24 @@ def floor_bound(floor, key):
 
 def llama_floor(w, inp, c, dy, batch, seq):
     """Per-tensor deviation (max |.| / max |ref|) of the bf16-emulated run
-    from the oracle on x[:batch, :seq]: {'y': e, (l, a, name): e}."""
+    from the oracle on x[:batch, :seq]: {'y': e, 'dx': e (c < 0),
+    (l, a, name): e}."""
     desc = oracle_desc(w)
     W, A = to64(inp, w)
     x = np.asarray(inp["x"], np.float64)[:batch, :seq]
     dy = np.asarray(dy, np.float64)[:batch, :seq]
     Bb, S, d = x.shape
     y_ref, c_ref = O.stage_forward(desc, W, A, x)
-    _, g_ref = O.stage_backward(desc, W, A, c_ref, dy, c)
+    dx_ref, g_ref = O.stage_backward(desc, W, A, c_ref, dy, c)
     h = x.reshape(Bb * S, d)
     caches = []
     for l in range(w.n_blocks):
         h, cache = llama_block_fwd_bf16(desc, W[l], A[l], h, Bb, S)
         caches.append(cache)
-    _, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
+    dx_emu, g_emu = O.stage_backward(desc, W, A, caches, dy, c)
     out = {"y": rel_err(h.reshape(Bb, S, d), y_ref)}
+    if c < 0:
+        out["dx"] = rel_err(dx_emu, dx_ref)
     for l in range(max(c, 0), w.n_blocks):
         for a in range(2):
             for k in ("w_down", "w_up"):

@@ -281,6 +281,45 @@ def test_llama_share_parity_on_a_causal_prefix(torch):
         assert e <= bound, (key, e, bound)
 
 
+# d > 1024: the split-K down projection, the feature-chunked up projection
+# and the separate row norms of the wide adapter path; T = 82 / 74 / 46
+# tokens is not a multiple of the 16-token tiles.
+WIDE = {
+    "wide_llama_d2048": Workload("wide_llama_d2048", "llama", "bf16", 2, 2048, 16, 512, 64, 41, 2, 1, "dy",
+                                 2008),
+    "wide_bert_single_d2048": Workload("wide_bert_single_d2048", "bert", "bf16", 2, 2048, 16, 512, 64, 37, 2, 1,
+                                       "dy", 2009, placement="ffn"),
+    "wide_bert_d3072": Workload("wide_bert_d3072", "bert", "bf16", 2, 3072, 24, 256, 64, 23, 2, 0, "dy", 2010),
+}
+
+
+@pytest.mark.parametrize("name", sorted(WIDE))
+def test_wide_adapter_parity(torch, name):
+    """Bound per tensor: max(2e-2, twice its bf16 storage floor)."""
+    from bf16_floor import bert_floor, llama_floor
+    w = WIDE[name]
+    inp = make_inputs(w)
+    st = Stage(w, inp)
+    try:
+        for c in (w.lowest_unfrozen, -1):
+            print(f"[{name}] c={c}", flush=True)
+            gpu = run_gpu(torch, st, w, inp, c, want_dx=(c < 0))
+            ref = oracle_run(w, inp, c)
+            fl = (llama_floor(w, inp, c, inp["dy"], w.batch, w.seq) if w.arch == "llama"
+                  else bert_floor(w, inp, c, ref))
+            bound = lambda key: max(2e-2, 2.0 * fl[key])
+            e = rel_err(gpu["y"], ref["y"])
+            print(f"[{name}] c={c} y error {e:.3e} (floor {fl['y']:.3e})", flush=True)
+            assert e <= bound("y")
+            check_grads(gpu, ref, max(c, 0), w.n_blocks, bound, name)
+            if c < 0:
+                e = rel_err(gpu["dx"], ref["dx"])
+                print(f"[{name}] dx error {e:.3e} (floor {fl['dx']:.3e})", flush=True)
+                assert e <= bound("dx")
+    finally:
+        st.close()
+
+
 def test_state_machine_and_workspace_errors(torch):
     w = SMALL["small_bert"]
     inp = make_inputs(w)
