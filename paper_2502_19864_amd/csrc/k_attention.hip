@@ -22,9 +22,12 @@ namespace rg {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
-__device__ __forceinline__ void rope_cs(int pos, int i, int dh, float log2theta, float* c, float* s) {
-  const float inv_freq = exp2f(-(2.f * (float)i / (float)dh) * log2theta);
-  sincosf((float)pos * inv_freq, s, c);
+// cos and sin of the rotation angle pos * theta^(-2i/dh) of pair i, from the
+// stage's table [max_seq][dh/2] (computed once in double precision)
+__device__ __forceinline__ void rope_cs(const float2* tab, int pos, int i, int dh, float* c, float* s) {
+  const float2 v = tab[(long)pos * (dh / 2) + i];
+  *c = v.x;
+  *s = v.y;
 }
 
 // ================================================================ bf16 / MFMA
@@ -37,7 +40,7 @@ constexpr int KT = 128;      // keys (or queries) per LDS tile: a whole 128-toke
 template <int DH, int NT>
 __device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int col0, bool rot0, bf16* dst0,
                                                const bf16* src1, int ld1, int col1, bf16* dst1, int b, int S,
-                                               int r0, float log2theta) {
+                                               int r0, const float2* rtab) {
   constexpr int HC = DH / 16;
   constexpr int PAIRS = KT * HC, IT = PAIRS / NT;
   static_assert(PAIRS % NT == 0, "whole passes of the workgroup");
@@ -68,7 +71,7 @@ __device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int co
 #pragma unroll
       for (int v = 0; v < 8; ++v) {
         float cs, sn;
-        rope_cs(row, c * 8 + v, DH, log2theta, &cs, &sn);
+        rope_cs(rtab, row, c * 8 + v, DH, &cs, &sn);
         const float a = x1[v], bb = x2[v];
         x1[v] = a * cs - bb * sn;
         x2[v] = bb * cs + a * sn;
@@ -87,7 +90,7 @@ __device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int co
 // 16s + 8*(lane/32) + v, rotated when rot.
 template <int DH>
 __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool valid, bool rot,
-                                               float log2theta, int half, bf16x8 f[DH / 16]) {
+                                               const float2* rtab, int half, bf16x8 f[DH / 16]) {
   float x[DH / 16][8];
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
@@ -102,7 +105,7 @@ __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool va
 #pragma unroll
       for (int v = 0; v < 8; ++v) {
         float cs, sn;
-        rope_cs(pos, 16 * s + 8 * half + v, DH, log2theta, &cs, &sn);
+        rope_cs(rtab, pos, 16 * s + 8 * half + v, DH, &cs, &sn);
         const float a = x[s][v], bb = x[s + DH / 32][v];
         x[s][v] = a * cs - bb * sn;
         x[s + DH / 32][v] = bb * cs + a * sn;
@@ -136,7 +139,7 @@ __device__ __forceinline__ int perm_pos(int r, int half) { return 8 * (r >> 2) +
 // 8*(r/4) + 4*half + r%4 of block db) scaled, optionally un-rotated.
 template <int DH>
 __device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, bool unrot, int pos,
-                                           float log2theta, int half, bf16* dst) {
+                                           const float2* rtab, int half, bf16* dst) {
   if (unrot) {
 #pragma unroll
     for (int db = 0; db < DH / 64; ++db)
@@ -144,7 +147,7 @@ __device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, 
       for (int r = 0; r < 16; ++r) {
         const int i = db * 32 + perm_pos(r, half);
         float cs, sn;
-        rope_cs(pos, i, DH, log2theta, &cs, &sn);
+        rope_cs(rtab, pos, i, DH, &cs, &sn);
         const float d1 = acc[db][r], d2 = acc[db + DH / 64][r];
         acc[db][r] = d1 * cs + d2 * sn;
         acc[db + DH / 64][r] = d2 * cs - d1 * sn;
@@ -170,13 +173,13 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
-  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float2* rtab = a.rope_tab;
   const float sl2 = kLog2e * rsqrtf((float)DH);
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
 
   bf16x8 qf[DH / 16];
   load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * DH, q, qv, a.rope,
-                     log2theta, half, qf);
+                     rtab, half, qf);
 
   f32x16 oacc[DH / 32];
 #pragma unroll
@@ -190,7 +193,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
     load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
-                                kt * KT, log2theta);
+                                kt * KT, rtab);
     __syncthreads();
     f32x16 sc[KT / 32];
 #pragma unroll
@@ -251,7 +254,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   }
   if (qv) {
     bf16* o = static_cast<bf16*>(a.o) + (long)(b * S + q) * a.ld_o + hd * DH;
-    store_rows<DH>(oacc, 1.f / lrun, false, q, 0.f, half, o);
+    store_rows<DH>(oacc, 1.f / lrun, false, q, nullptr, half, o);
     if (half == 0) a.lse[(long)bh * S + q] = mrun + log2f(lrun);
   }
 }
@@ -266,15 +269,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
-  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float2* rtab = a.rope_tab;
   const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const long qrow = (long)(b * S + (qv ? q : 0));
 
   bf16x8 qf[DH / 16], df[DH / 16];
-  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * DH, q, qv, a.rope, log2theta, half, qf);
+  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * DH, q, qv, a.rope, rtab, half, qf);
   load_row_frags<DH>(static_cast<const bf16*>(a.dout) + qrow * a.ld_do + hd * DH, q, qv, false,
-                     0.f, half, df);
+                     nullptr, half, df);
   float dsum = 0.f;
   {
     const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
@@ -306,7 +309,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
     load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
-                                kt * KT, log2theta);
+                                kt * KT, rtab);
     __syncthreads();
     // one key block at a time (not unrolled): keeps the kernel within the
     // registers of two waves per SIMD, so a (batch, head) grid fits one round
@@ -338,7 +341,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   }
   if (qv) {
     bf16* dst = static_cast<bf16*>(a.dqkv) + (long)(b * S + q) * a.ld_dqkv + hd * DH;
-    store_rows<DH>(dq, scale, a.rope, q, log2theta, half, dst);
+    store_rows<DH>(dq, scale, a.rope, q, rtab, half, dst);
   }
 }
 
@@ -353,15 +356,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const int key = blockIdx.x * (32 * NW) + wave * 32 + l32;
   const bool kv = key < S;
   const int d = a.H * DH;
-  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float2* rtab = a.rope_tab;
   const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const bf16* dO = static_cast<const bf16*>(a.dout);
   const long krow = (long)(b * S + (kv ? key : 0));
 
   bf16x8 kf[DH / 16], vf[DH / 16];
-  load_row_frags<DH>(qkv + krow * a.ld_qkv + d + hd * DH, key, kv, a.rope, log2theta, half, kf);
-  load_row_frags<DH>(qkv + krow * a.ld_qkv + 2 * d + hd * DH, key, kv, false, 0.f, half, vf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + d + hd * DH, key, kv, a.rope, rtab, half, kf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + 2 * d + hd * DH, key, kv, false, nullptr, half, vf);
 
   f32x16 dk[DH / 32], dv[DH / 32];
 #pragma unroll
@@ -376,7 +379,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
     load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
-                                log2theta);
+                                rtab);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
       sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
@@ -416,8 +419,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   }
   if (kv) {
     bf16* dst = static_cast<bf16*>(a.dqkv) + (long)(b * S + key) * a.ld_dqkv;
-    store_rows<DH>(dk, scale, a.rope, key, log2theta, half, dst + d + hd * DH);
-    store_rows<DH>(dv, 1.f, false, key, 0.f, half, dst + 2 * d + hd * DH);
+    store_rows<DH>(dk, scale, a.rope, key, rtab, half, dst + d + hd * DH);
+    store_rows<DH>(dv, 1.f, false, key, nullptr, half, dst + 2 * d + hd * DH);
   }
 }
 
@@ -425,30 +428,30 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 // One workgroup per (batch, head), one thread per query (forward, dQ) or key
 // (dK, dV); head dim <= 128.
 __device__ __forceinline__ float rot_ld(const float* row, int i, int dh, int pos, bool rot,
-                                        float log2theta) {
+                                        const float2* rtab) {
   if (!rot) return row[i];
   const int h2 = dh / 2, j = i < h2 ? i : i - h2;
   float cs, sn;
-  rope_cs(pos, j, dh, log2theta, &cs, &sn);
+  rope_cs(rtab, pos, j, dh, &cs, &sn);
   const float x1 = row[j], x2 = row[j + h2];
   return i < h2 ? x1 * cs - x2 * sn : x2 * cs + x1 * sn;
 }
 
 __global__ __launch_bounds__(256) void attn_fwd_f32(AttnArgs a) {
   const int bh = blockIdx.x, b = bh / a.H, hd = bh % a.H, S = a.S, DH = a.dh, d = a.H * DH;
-  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float2* rtab = a.rope_tab;
   const float sl2 = kLog2e * rsqrtf((float)DH);
   const float* qkv = static_cast<const float*>(a.qkv);
   for (int q = threadIdx.x; q < S; q += blockDim.x) {
     const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
     float qv[128];
-    for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, log2theta);
+    for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, rtab);
     const int kend = a.causal ? q + 1 : S;
     float m = -INFINITY;
     for (int k = 0; k < kend; ++k) {
       const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
       float sdot = 0.f;
-      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, rtab);
       m = fmaxf(m, sdot * sl2);
     }
     float l = 0.f, o[128];
@@ -457,7 +460,7 @@ __global__ __launch_bounds__(256) void attn_fwd_f32(AttnArgs a) {
       const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
       const float* vr = kr + d;
       float sdot = 0.f;
-      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+      for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, rtab);
       const float p = exp2f(sdot * sl2 - m);
       l += p;
       for (int i = 0; i < DH; ++i) o[i] += p * vr[i];
@@ -471,7 +474,7 @@ __global__ __launch_bounds__(256) void attn_fwd_f32(AttnArgs a) {
 __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
   extern __shared__ float sD[];  // [S]
   const int bh = blockIdx.x, b = bh / a.H, hd = bh % a.H, S = a.S, DH = a.dh, d = a.H * DH;
-  const float log2theta = a.rope ? log2f(a.theta) : 0.f;
+  const float2* rtab = a.rope_tab;
   const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
   const float* qkv = static_cast<const float*>(a.qkv);
   const float* O = static_cast<const float*>(a.o);
@@ -480,7 +483,7 @@ __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
   auto score = [&](int q, int k, const float* qv) {
     const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
     float sdot = 0.f;
-    for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, log2theta);
+    for (int i = 0; i < DH; ++i) sdot += qv[i] * rot_ld(kr, i, DH, k, a.rope, rtab);
     return exp2f(sdot * sl2 - a.lse[(long)bh * S + q]);
   };
   auto dpdot = [&](int q, int k) {
@@ -503,19 +506,19 @@ __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
   // dQ
   for (int q = threadIdx.x; q < S; q += blockDim.x) {
     const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
-    for (int i = 0; i < DH; ++i) { buf[i] = rot_ld(qr, i, DH, q, a.rope, log2theta); acc[i] = 0.f; }
+    for (int i = 0; i < DH; ++i) { buf[i] = rot_ld(qr, i, DH, q, a.rope, rtab); acc[i] = 0.f; }
     const int kend = a.causal ? q + 1 : S;
     for (int k = 0; k < kend; ++k) {
       const float ds = score(q, k, buf) * (dpdot(q, k) - sD[q]);
       const float* kr = qkv + (long)(b * S + k) * a.ld_qkv + d + hd * DH;
-      for (int i = 0; i < DH; ++i) acc[i] += ds * rot_ld(kr, i, DH, k, a.rope, log2theta);
+      for (int i = 0; i < DH; ++i) acc[i] += ds * rot_ld(kr, i, DH, k, a.rope, rtab);
     }
     float* dst = dqkv + (long)(b * S + q) * a.ld_dqkv + hd * DH;
     for (int i = 0; i < DH; ++i) acc[i] *= scale;
     if (a.rope) {
       for (int j = 0; j < DH / 2; ++j) {
         float cs, sn;
-        rope_cs(q, j, DH, log2theta, &cs, &sn);
+        rope_cs(rtab, q, j, DH, &cs, &sn);
         const float d1 = acc[j], d2 = acc[j + DH / 2];
         acc[j] = d1 * cs + d2 * sn;
         acc[j + DH / 2] = d2 * cs - d1 * sn;
@@ -530,7 +533,7 @@ __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
     for (int q = qbeg; q < S; ++q) {
       const float* qr = qkv + (long)(b * S + q) * a.ld_qkv + hd * DH;
       float qv[128];
-      for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, log2theta);
+      for (int i = 0; i < DH; ++i) qv[i] = rot_ld(qr, i, DH, q, a.rope, rtab);
       const float p = score(q, k, qv);
       const float ds = p * (dpdot(q, k) - sD[q]);
       const float* dr = dO + (long)(b * S + q) * a.ld_do + hd * DH;
@@ -541,7 +544,7 @@ __global__ __launch_bounds__(256) void attn_bwd_f32(AttnArgs a) {
     if (a.rope) {
       for (int j = 0; j < DH / 2; ++j) {
         float cs, sn;
-        rope_cs(k, j, DH, log2theta, &cs, &sn);
+        rope_cs(rtab, k, j, DH, &cs, &sn);
         const float d1 = acc[j], d2 = acc[j + DH / 2];
         acc[j] = d1 * cs + d2 * sn;
         acc[j + DH / 2] = d2 * cs - d1 * sn;
@@ -580,6 +583,7 @@ static hipError_t bwd_dh(const AttnArgs& a, hipStream_t s) {
 static hipError_t check(int dtype, const AttnArgs& a, bool bwd) {
   if (a.B <= 0 || a.S <= 0 || a.H <= 0 || !a.qkv || !a.o || !a.lse) return hipErrorInvalidValue;
   if (bwd && (!a.dout || !a.dsum || !a.dqkv)) return hipErrorInvalidValue;
+  if (a.rope && (!a.rope_tab || a.rope_rows < a.S)) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
     if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
     if (a.ld_qkv % 8 || a.ld_o % 8 || !al16(a.qkv) || !al16(a.o)) return hipErrorInvalidValue;

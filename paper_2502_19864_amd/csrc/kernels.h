@@ -70,6 +70,8 @@ struct AttnArgs {
   int B, S, H, dh;
   int causal, rope;
   float theta;
+  const float2* rope_tab;       // rope: (cos, sin) of pos * theta^(-2i/dh), [rope_rows][dh/2]
+  int rope_rows;                // positions the table covers (>= S)
   const void* qkv; int ld_qkv;  // [B*S, ld] with Q at column 0, K at d, V at 2d
   void* o; int ld_o;            // [B*S, d]
   float* lse;                   // [B, H, S]

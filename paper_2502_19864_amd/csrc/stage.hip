@@ -6,6 +6,7 @@
 #include <string.h>
 
 #include <algorithm>
+#include <cmath>
 #include <limits>
 #include <string>
 #include <vector>
@@ -248,6 +249,7 @@ struct ringada_stage {
   std::vector<BlockBind> blocks;
   std::vector<void*> allocs;
   AdapterSlot* slots_dev = nullptr;
+  float2* rope_tab = nullptr;  // rotary (cos, sin) [max_seq][d_head/2], built at the first bind
   std::vector<AdapterSlot> slots;
   // state machine
   bool pending = false;
@@ -322,6 +324,17 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
       for (int k = 0; k < 4; ++k) RG_TRY(dalloc(st, d * m * es, &b.wk[a][k]));
   }
   if (!st->slots_dev) RG_TRY(dalloc(st, st->slots.size() * sizeof(AdapterSlot), (void**)&st->slots_dev));
+  if (!post && !st->rope_tab) {  // rotation angles pos * theta^(-2i/dh), in double, once per stage
+    const int dh = (int)(d / D.n_heads), half = dh / 2;
+    std::vector<float2> tab((size_t)D.max_seq * half);
+    for (int p = 0; p < D.max_seq; ++p)
+      for (int i = 0; i < half; ++i) {
+        const double ang = p * std::pow((double)D.rope_theta, -2.0 * i / dh);
+        tab[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
+      }
+    RG_TRY(dalloc(st, tab.size() * sizeof(float2), (void**)&st->rope_tab));
+    RG_HIP(hipMemcpy(st->rope_tab, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice));
+  }
   b.w = *w;
   b.ad[0] = attn ? *attn : ringada_adapter{};
   b.ad[1] = *ffn;
@@ -486,6 +499,7 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
   AttnArgs aa{};
   aa.B = L.B; aa.S = L.S; aa.H = c.H; aa.dh = c.dh;
   aa.causal = c.llama; aa.rope = c.llama; aa.theta = st->D.rope_theta;
+  aa.rope_tab = st->rope_tab; aa.rope_rows = st->D.max_seq;
   aa.qkv = qkv; aa.ld_qkv = 3 * d; aa.o = o; aa.ld_o = d; aa.lse = lse;
   const double attn_flops = 4.0 * L.B * c.H * (double)L.S * L.S * c.dh * (c.llama ? 0.5 : 1.0);
   RG_TRY(run(st, c.s, "attn_fwd", attn_flops, es * 4.0 * T * d, [&] { return launch_attn_fwd(c.dt, aa, c.s); }));
@@ -665,6 +679,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   AttnArgs at{};
   at.B = L.B; at.S = L.S; at.H = c.H; at.dh = c.dh;
   at.causal = c.llama; at.rope = c.llama; at.theta = st->D.rope_theta;
+  at.rope_tab = st->rope_tab; at.rope_rows = st->D.max_seq;
   at.qkv = c.S(sb.qkv); at.ld_qkv = 3 * d; at.o = c.S(sb.o); at.ld_o = d;
   at.lse = static_cast<float*>(c.S(sb.lse));
   at.dout = c.W(L.dout); at.ld_do = d; at.dsum = static_cast<float*>(c.W(L.dsum));
