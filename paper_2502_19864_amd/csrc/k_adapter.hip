@@ -443,7 +443,8 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
 //          G = S * gelu'(u) backward (G written as du); then, per chunk of
 //          WIDE_UC features, out = Z [+ R] + G W^T, W in the B fragment layout
 //          (W_up^T forward, W_down backward); grid (T/16) x (d/WIDE_UC);
-//   norm:  a row kernel for LayerNorm / RMSNorm forward or backward.
+//   norm:  the vectorised row kernels for LayerNorm / RMSNorm forward or
+//          backward (launch_norm_rows_fwd / _bwd).
 // Both MFMA kernels use 16x16x32 with the weight as the A operand, as the row
 // kernels do, and read every operand fragment straight from global memory
 // (one contiguous 1-KB run per packed weight fragment).
@@ -553,128 +554,6 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
       o[q] = acc[q] + zf + rf;
     }
     St<bf16>::st4(out, row + (b0 + b) * 16 + 4 * grp, o);
-  }
-}
-
-// Row norms for wide widths: one 256-thread workgroup per token, eight
-// features per 16-B access (d <= 4096, so at most two per thread).
-constexpr int WIDE_NPT = 2;
-__device__ __forceinline__ float block_sum256(float v, float* red) {
-  v = wave_sum(v);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) red[wave] = v;
-  __syncthreads();
-  const float t = (red[0] + red[1]) + (red[2] + red[3]);
-  __syncthreads();
-  return t;
-}
-__device__ __forceinline__ void ld8f(const bf16* p, float v[8]) { unpack_frag(ld_frag(p), v); }
-__device__ __forceinline__ void st8f(bf16* p, const float v[8]) { *reinterpret_cast<bf16x8*>(p) = pack_frag(v); }
-
-// h = x1 (+ x2); LN: out = LN(h) g + b (out may alias x1); RMS: out = h (when
-// x2 is given) and out_norm = RMSNorm(h) g; None: out = h.  xhat, rstd stashed
-// when given.
-__global__ __launch_bounds__(256) void adapter_wide_norm_fwd(int d, float eps, Norm norm, const bf16* x1,
-                                                             const bf16* x2, const bf16* gamma, const bf16* beta,
-                                                             bf16* out, bf16* out_norm, bf16* xhat, float* rstd) {
-  __shared__ float red[4];
-  const long row = (long)blockIdx.x * d;
-  const int nc = d / 8;
-  float v[WIDE_NPT][8];
-#pragma unroll
-  for (int i = 0; i < WIDE_NPT; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c >= nc) continue;
-    ld8f(x1 + row + 8 * c, v[i]);
-    if (x2) {
-      float y[8];
-      ld8f(x2 + row + 8 * c, y);
-#pragma unroll
-      for (int q = 0; q < 8; ++q) v[i][q] += y[q];
-    }
-  }
-  if (norm == Norm::None || (norm == Norm::RMS && x2)) {
-#pragma unroll
-    for (int i = 0; i < WIDE_NPT; ++i) {
-      const int c = threadIdx.x + 256 * i;
-      if (c < nc) st8f(out + row + 8 * c, v[i]);
-    }
-    if (norm == Norm::None) return;
-  }
-  float mean = 0.f;
-  if (norm == Norm::LN) {
-    float s = 0.f;
-#pragma unroll
-    for (int i = 0; i < WIDE_NPT; ++i)
-      if (threadIdx.x + 256 * i < nc)
-#pragma unroll
-        for (int q = 0; q < 8; ++q) s += v[i][q];
-    mean = block_sum256(s, red) / (float)d;
-  }
-  float s2 = 0.f;
-#pragma unroll
-  for (int i = 0; i < WIDE_NPT; ++i)
-    if (threadIdx.x + 256 * i < nc)
-#pragma unroll
-      for (int q = 0; q < 8; ++q) {
-        const float c = v[i][q] - mean;
-        s2 += c * c;
-      }
-  const float rs = rsqrtf(block_sum256(s2, red) / (float)d + eps);
-  if (rstd && threadIdx.x == 0) rstd[blockIdx.x] = rs;
-  bf16* dst = norm == Norm::LN ? out : out_norm;
-#pragma unroll
-  for (int i = 0; i < WIDE_NPT; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c >= nc) continue;
-    float xh[8], g[8], b[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
-    ld8f(gamma + 8 * c, g);
-    if (norm == Norm::LN) ld8f(beta + 8 * c, b);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      xh[q] = (v[i][q] - mean) * rs;
-      o[q] = xh[q] * g[q] + b[q];
-    }
-    st8f(dst + row + 8 * c, o);
-    if (xhat) st8f(xhat + row + 8 * c, xh);
-  }
-}
-
-// dz = [dres +] rstd (g*gin - [mean(g*gin)] - xhat mean(g*gin*xhat)), LN or RMS
-__global__ __launch_bounds__(256) void adapter_wide_norm_bwd(int d, Norm norm, const bf16* gin, const bf16* xhat,
-                                                             const float* rstd, const bf16* gamma,
-                                                             const bf16* dres, bf16* dz) {
-  __shared__ float red[4];
-  const long row = (long)blockIdx.x * d;
-  const int nc = d / 8;
-  float gg[WIDE_NPT][8], xh[WIDE_NPT][8];
-  float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-  for (int i = 0; i < WIDE_NPT; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c >= nc) continue;
-    float g[8];
-    ld8f(gin + row + 8 * c, gg[i]);
-    ld8f(xhat + row + 8 * c, xh[i]);
-    ld8f(gamma + 8 * c, g);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) {
-      gg[i][q] *= g[q];
-      s1 += gg[i][q];
-      s2 += gg[i][q] * xh[i][q];
-    }
-  }
-  const float m1 = norm == Norm::LN ? block_sum256(s1, red) / (float)d : 0.f;
-  const float m2 = block_sum256(s2, red) / (float)d, rs = rstd[blockIdx.x];
-#pragma unroll
-  for (int i = 0; i < WIDE_NPT; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c >= nc) continue;
-    float r[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
-    if (norm == Norm::RMS) ld8f(dres + row + 8 * c, r);
-#pragma unroll
-    for (int q = 0; q < 8; ++q) o[q] = r[q] + rs * (gg[i][q] - m1 - xh[i][q] * m2);
-    st8f(dz + row + 8 * c, o);
   }
 }
 
@@ -865,7 +744,7 @@ long adapter_part_elems(int dtype, int T, int d, int m) {
 }
 
 static hipError_t fwd_wide(const AdapterFwdArgs& a, hipStream_t s) {
-  if (a.d % WIDE_KC || a.d / 8 > 256 * WIDE_NPT || (a.wdn_t && !a.part)) return hipErrorInvalidValue;
+  if (a.d % WIDE_KC || a.d > 4096 || (a.wdn_t && !a.part)) return hipErrorInvalidValue;
   for (const void* p : std::initializer_list<const void*>{a.z, a.res, a.out, a.out_norm, a.xhat, a.gamma, a.beta})  // 16-B row accesses
     if (p && !al16(p)) return hipErrorInvalidValue;
   const bf16* z = static_cast<const bf16*>(a.z);
@@ -878,26 +757,22 @@ static hipError_t fwd_wide(const AdapterFwdArgs& a, hipStream_t s) {
     RG_LAUNCH((adapter_wide_up<false>), dim3(ntok, nuc), dim3(256), 0, s, a.part, nkc, nullptr,
               static_cast<bf16*>(a.u), a.T, a.d, static_cast<const bf16*>(a.wup_t), z, res, out);
     if (a.norm != Norm::None)  // the norm of h, now in out
-      RG_LAUNCH(adapter_wide_norm_fwd, dim3(a.T), dim3(256), 0, s, a.d, a.eps, a.norm, out, nullptr,
-                static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.beta), out,
-                static_cast<bf16*>(a.out_norm), static_cast<bf16*>(a.xhat), a.rstd);
-  } else {
-    RG_LAUNCH(adapter_wide_norm_fwd, dim3(a.T), dim3(256), 0, s, a.d, a.eps, a.norm, z, res,
-              static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.beta), out,
-              static_cast<bf16*>(a.out_norm), static_cast<bf16*>(a.xhat), a.rstd);
+      return launch_norm_rows_fwd(a.T, a.d, a.eps, a.norm, out, nullptr, a.gamma, a.beta, out, a.out_norm, a.xhat,
+                                  a.rstd, s);
+    return hipGetLastError();
   }
-  return hipGetLastError();
+  return launch_norm_rows_fwd(a.T, a.d, a.eps, a.norm, z, res, a.gamma, a.beta, out, a.out_norm, a.xhat, a.rstd, s);
 }
 
 static hipError_t bwd_wide(const AdapterBwdArgs& a, hipStream_t s) {
   const bool has_ad = a.wup != nullptr;
-  if (a.d % WIDE_KC || a.d / 8 > 256 * WIDE_NPT || (has_ad && !a.part)) return hipErrorInvalidValue;
+  if (a.d % WIDE_KC || a.d > 4096 || (has_ad && !a.part)) return hipErrorInvalidValue;
   for (const void* p : std::initializer_list<const void*>{a.gin, a.dres, a.xhat, a.gamma, a.dz, a.dzin})  // 16-B row accesses
     if (p && !al16(p)) return hipErrorInvalidValue;
   const bf16* dZ = static_cast<const bf16*>(a.gin);
   if (a.norm != Norm::None) {
-    RG_LAUNCH(adapter_wide_norm_bwd, dim3(a.T), dim3(256), 0, s, a.d, a.norm, dZ, static_cast<const bf16*>(a.xhat),
-              a.rstd, static_cast<const bf16*>(a.gamma), static_cast<const bf16*>(a.dres), static_cast<bf16*>(a.dz));
+    const hipError_t e = launch_norm_rows_bwd(a.T, a.d, a.norm, dZ, a.xhat, a.rstd, a.gamma, a.dres, a.dz, s);
+    if (e != hipSuccess) return e;
     dZ = static_cast<const bf16*>(a.dz);
   } else if (a.dz && a.dz != a.gin) {  // no norm: the adapter-output gradient is gin itself
     const hipError_t e = hipMemcpyAsync(a.dz, a.gin, (size_t)a.T * a.d * 2, hipMemcpyDeviceToDevice, s);

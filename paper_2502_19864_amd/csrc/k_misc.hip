@@ -1,6 +1,8 @@
-// Row-wise RMSNorm, parameter layout kernels, the adapter update and the
+// Row-wise norms (RMSNorm, and the vectorised LayerNorm / RMSNorm rows of the
+// wide adapters), parameter layout kernels, the adapter update and the
 // initiator's loss helpers.
 #include <algorithm>
+#include <initializer_list>
 #include <type_traits>
 
 #include "common.h"
@@ -55,10 +57,168 @@ __global__ __launch_bounds__(256) void rms_bwd_k(int d, const T* dn, const T* dr
   }
 }
 
+// ---------------------------------------------------------------- row norms, bf16, vectorised
+// One 256-thread workgroup per row, eight features per 16-B access (d <= 4096,
+// so at most two per thread).
+constexpr int NORM_NPT = 2;
+__device__ __forceinline__ float block_sum256(float v, float* red) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) red[wave] = v;
+  __syncthreads();
+  const float t = (red[0] + red[1]) + (red[2] + red[3]);
+  __syncthreads();
+  return t;
+}
+__device__ __forceinline__ void ld8f(const bf16* p, float v[8]) { unpack_frag(ld_frag(p), v); }
+__device__ __forceinline__ void st8f(bf16* p, const float v[8]) { *reinterpret_cast<bf16x8*>(p) = pack_frag(v); }
+
+// h = x1 (+ x2); LN: out = LN(h) g + b (out may alias x1); RMS: out = h (when
+// x2 is given) and out_norm = RMSNorm(h) g; None: out = h.  xhat, rstd stashed
+// when given.
+__global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm norm, const bf16* x1,
+                                                             const bf16* x2, const bf16* gamma, const bf16* beta,
+                                                             bf16* out, bf16* out_norm, bf16* xhat, float* rstd) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  const int nc = d / 8;
+  float v[NORM_NPT][8];
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    ld8f(x1 + row + 8 * c, v[i]);
+    if (x2) {
+      float y[8];
+      ld8f(x2 + row + 8 * c, y);
+#pragma unroll
+      for (int q = 0; q < 8; ++q) v[i][q] += y[q];
+    }
+  }
+  if (norm == Norm::None || (norm == Norm::RMS && x2)) {
+#pragma unroll
+    for (int i = 0; i < NORM_NPT; ++i) {
+      const int c = threadIdx.x + 256 * i;
+      if (c < nc) st8f(out + row + 8 * c, v[i]);
+    }
+    if (norm == Norm::None) return;
+  }
+  float mean = 0.f;
+  if (norm == Norm::LN) {
+    float s = 0.f;
+#pragma unroll
+    for (int i = 0; i < NORM_NPT; ++i)
+      if (threadIdx.x + 256 * i < nc)
+#pragma unroll
+        for (int q = 0; q < 8; ++q) s += v[i][q];
+    mean = block_sum256(s, red) / (float)d;
+  }
+  float s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i)
+    if (threadIdx.x + 256 * i < nc)
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float c = v[i][q] - mean;
+        s2 += c * c;
+      }
+  const float rs = rsqrtf(block_sum256(s2, red) / (float)d + eps);
+  if (rstd && threadIdx.x == 0) rstd[blockIdx.x] = rs;
+  bf16* dst = norm == Norm::LN ? out : out_norm;
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float xh[8], g[8], b[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
+    ld8f(gamma + 8 * c, g);
+    if (norm == Norm::LN) ld8f(beta + 8 * c, b);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      xh[q] = (v[i][q] - mean) * rs;
+      o[q] = xh[q] * g[q] + b[q];
+    }
+    st8f(dst + row + 8 * c, o);
+    if (xhat) st8f(xhat + row + 8 * c, xh);
+  }
+}
+
+// dz = [dres +] rstd (g*gin - [mean(g*gin)] - xhat mean(g*gin*xhat)), LN or RMS
+__global__ __launch_bounds__(256) void norm_rows_bwd_bf16(int d, Norm norm, const bf16* gin, const bf16* xhat,
+                                                             const float* rstd, const bf16* gamma,
+                                                             const bf16* dres, bf16* dz) {
+  __shared__ float red[4];
+  const long row = (long)blockIdx.x * d;
+  const int nc = d / 8;
+  float gg[NORM_NPT][8], xh[NORM_NPT][8];
+  float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float g[8];
+    ld8f(gin + row + 8 * c, gg[i]);
+    ld8f(xhat + row + 8 * c, xh[i]);
+    ld8f(gamma + 8 * c, g);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) {
+      gg[i][q] *= g[q];
+      s1 += gg[i][q];
+      s2 += gg[i][q] * xh[i][q];
+    }
+  }
+  const float m1 = norm == Norm::LN ? block_sum256(s1, red) / (float)d : 0.f;
+  const float m2 = block_sum256(s2, red) / (float)d, rs = rstd[blockIdx.x];
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i;
+    if (c >= nc) continue;
+    float r[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
+    if (norm == Norm::RMS) ld8f(dres + row + 8 * c, r);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o[q] = r[q] + rs * (gg[i][q] - m1 - xh[i][q] * m2);
+    st8f(dz + row + 8 * c, o);
+  }
+}
+
+static bool al16p(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+hipError_t launch_norm_rows_fwd(int T, int d, float eps, Norm norm, const void* x1, const void* x2, const void* gamma,
+                                const void* beta, void* out, void* out_norm, void* xhat, float* rstd, hipStream_t s) {
+  if (T < 0 || d <= 0 || d % 8 || d > 256 * 8 * NORM_NPT || !x1) return hipErrorInvalidValue;
+  if (norm != Norm::None && !gamma) return hipErrorInvalidValue;
+  if (norm == Norm::LN && (!beta || !out)) return hipErrorInvalidValue;
+  if (norm == Norm::RMS && !out_norm) return hipErrorInvalidValue;
+  if ((norm == Norm::None || (norm == Norm::RMS && x2)) && !out) return hipErrorInvalidValue;
+  for (const void* p : {x1, x2, gamma, beta, static_cast<const void*>(out), static_cast<const void*>(out_norm),
+                        static_cast<const void*>(xhat)})
+    if (p && !al16p(p)) return hipErrorInvalidValue;
+  if (T == 0) return hipSuccess;
+  RG_LAUNCH(norm_rows_fwd_bf16, dim3(T), dim3(256), 0, s, d, eps, norm, static_cast<const bf16*>(x1),
+            static_cast<const bf16*>(x2), static_cast<const bf16*>(gamma), static_cast<const bf16*>(beta),
+            static_cast<bf16*>(out), static_cast<bf16*>(out_norm), static_cast<bf16*>(xhat), rstd);
+  return hipGetLastError();
+}
+
+hipError_t launch_norm_rows_bwd(int T, int d, Norm norm, const void* gin, const void* xhat, const float* rstd,
+                                const void* gamma, const void* dres, void* dz, hipStream_t s) {
+  if (T < 0 || d <= 0 || d % 8 || d > 256 * 8 * NORM_NPT || norm == Norm::None) return hipErrorInvalidValue;
+  if (!gin || !xhat || !rstd || !gamma || !dz || (norm == Norm::RMS && !dres)) return hipErrorInvalidValue;
+  for (const void* p : {gin, xhat, gamma, dres, static_cast<const void*>(dz)})
+    if (p && !al16p(p)) return hipErrorInvalidValue;
+  if (T == 0) return hipSuccess;
+  RG_LAUNCH(norm_rows_bwd_bf16, dim3(T), dim3(256), 0, s, d, norm, static_cast<const bf16*>(gin),
+            static_cast<const bf16*>(xhat), rstd, static_cast<const bf16*>(gamma), static_cast<const bf16*>(dres),
+            static_cast<bf16*>(dz));
+  return hipGetLastError();
+}
+
 hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g, void* out,
                           void* xhat, float* rstd, hipStream_t s) {
   if (T < 0 || d <= 0 || !x || !g || !out) return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
+  if (dtype == DT_BF16 && d % 8 == 0 && d <= 256 * 8 * NORM_NPT && al16p(x) && al16p(g) && al16p(out) &&
+      (!xhat || al16p(xhat)))
+    return launch_norm_rows_fwd(T, d, eps, Norm::RMS, x, nullptr, g, nullptr, nullptr, out, xhat, rstd, s);
   if (dtype == DT_BF16)
     RG_LAUNCH(rms_fwd_k<bf16>, dim3(T), dim3(256), 0, s, d, eps, (const bf16*)x,
                        (const bf16*)g, (bf16*)out, (bf16*)xhat, rstd);
@@ -72,6 +232,9 @@ hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* d
                           const float* rstd, const void* g, void* dx, hipStream_t s) {
   if (T < 0 || d <= 0 || !dn || !dres || !xhat || !rstd || !g || !dx) return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
+  if (dtype == DT_BF16 && d % 8 == 0 && d <= 256 * 8 * NORM_NPT && al16p(dn) && al16p(dres) && al16p(xhat) &&
+      al16p(g) && al16p(dx))
+    return launch_norm_rows_bwd(T, d, Norm::RMS, dn, xhat, rstd, g, dres, dx, s);
   if (dtype == DT_BF16)
     RG_LAUNCH(rms_bwd_k<bf16>, dim3(T), dim3(256), 0, s, d, (const bf16*)dn,
                        (const bf16*)dres, (const bf16*)xhat, rstd, (const bf16*)g, (bf16*)dx);

@@ -145,6 +145,16 @@ hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s);
 // out = RMSNorm(x) * g, xhat/rstd stashes optional
 hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g,
                           void* out, void* xhat, float* rstd, hipStream_t s);
+// bf16 rows, d % 8 == 0, d <= 4096, 16-B aligned rows: h = x1 (+ x2);
+// LN: out = LN(h) gamma + beta (out may alias x1); RMS: out = h when x2 is
+// given, out_norm = RMSNorm(h) gamma; None: out = h.  xhat / rstd stashed when
+// non-null.
+hipError_t launch_norm_rows_fwd(int T, int d, float eps, Norm norm, const void* x1, const void* x2,
+                                const void* gamma, const void* beta, void* out, void* out_norm, void* xhat,
+                                float* rstd, hipStream_t s);
+// dz = [dres +] rstd (gamma gin - [mean(gamma gin)] - xhat mean(gamma gin xhat)), LN or RMS
+hipError_t launch_norm_rows_bwd(int T, int d, Norm norm, const void* gin, const void* xhat, const float* rstd,
+                                const void* gamma, const void* dres, void* dz, hipStream_t s);
 // dx = dres + RMSNorm'(dn)
 hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* dres,
                           const void* xhat, const float* rstd, const void* g, void* dx,
