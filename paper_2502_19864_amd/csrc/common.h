@@ -176,6 +176,16 @@ __device__ __forceinline__ const bf16* pack_b_frag(const void* base, int d, int 
   return static_cast<const bf16*>(base) + ((long)(wave * 2 * (d / 256) + 2 * b + h) * 64 + lane) * 8;
 }
 
+// ---------------------------------------------------------------- XCD-aware block order
+// Workgroups are dispatched round-robin over the 8 XCDs (linear workgroup id i
+// runs on XCD i % 8), each XCD with its own L2.  xcd_block maps the linear id
+// of one of n workgroups to a block index such that every XCD processes a
+// contiguous eighth of the blocks (identity when n is not a multiple of 8).
+// The projection GEMMs give each XCD a contiguous band of token rows the same
+// way, so a kernel whose blocks are token ranges in this order finds the rows
+// the previous kernel wrote in its own XCD's L2.
+__device__ __forceinline__ int xcd_block(int id, int n) { return n % 8 == 0 ? (id % 8) * (n / 8) + id / 8 : id; }
+
 // ---------------------------------------------------------------- reductions
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

@@ -169,8 +169,9 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
+  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+  const int qb = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int q = qb * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
   const float2* rtab = a.rope_tab;
@@ -188,7 +189,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
     for (int r = 0; r < 16; ++r) oacc[i][r] = 0.f;
   float mrun = -INFINITY, lrun = 0.f;
 
-  const int qlast = min(S - 1, blockIdx.x * (32 * NW) + 32 * NW - 1);
+  const int qlast = min(S - 1, qb * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
@@ -265,8 +266,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int q = blockIdx.x * (32 * NW) + wave * 32 + l32;
+  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+  const int qb = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int q = qb * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
   const float2* rtab = a.rope_tab;
@@ -302,11 +304,11 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 #pragma unroll
     for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
 
-  const int qlast = min(S - 1, blockIdx.x * (32 * NW) + 32 * NW - 1);
+  const int qlast = min(S - 1, qb * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     // every query of the workgroup and every key of the tile in range, no causal mask
-    const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
+    const bool full = !CAUSAL && (qb + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
     load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
                                 kt * KT, rtab);
@@ -352,8 +354,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
   __shared__ float sL[KT], sD[KT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int bh = blockIdx.y, b = bh / a.H, hd = bh % a.H, S = a.S;
-  const int key = blockIdx.x * (32 * NW) + wave * 32 + l32;
+  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+  const int kb0 = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int key = kb0 * (32 * NW) + wave * 32 + l32;
   const bool kv = key < S;
   const int d = a.H * DH;
   const float2* rtab = a.rope_tab;
@@ -373,10 +376,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     for (int r = 0; r < 16; ++r) dk[i][r] = dv[i][r] = 0.f;
 
   const int nqt = (S + KT - 1) / KT;
-  const int qt0 = CAUSAL ? (blockIdx.x * (32 * NW)) / KT : 0;
+  const int qt0 = CAUSAL ? (kb0 * (32 * NW)) / KT : 0;
   for (int qt = qt0; qt < nqt; ++qt) {
     // every key of the workgroup and every query of the tile in range, no causal mask
-    const bool full = !CAUSAL && (int)(blockIdx.x + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
+    const bool full = !CAUSAL && (kb0 + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
     load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
                                 rtab);
