@@ -427,6 +427,157 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   }
 }
 
+// Whole backward of one (batch, head) with S <= KT (one query block, one key
+// tile), one workgroup: P and dS are formed once.  Wave w owns queries
+// 32w..32w+31 (lane = query, as in the dQ pass): it computes its score and
+// dP blocks against the K and V tiles, accumulates dQ and keeps P and dS
+// packed in registers.  The K/V tile space is then reused for P (row-major
+// [query][key]); each wave now owns keys 32w..32w+31 and reads its P^T
+// fragments from that block with the LDS transpose read, for dV = P^T dO;
+// then dS goes to the same space for dK = dS^T Q.  The LDS holds Q, dO and
+// the K/V tiles (74 KB at d_head 64: two workgroups per CU).
+template <int DH, bool CAUSAL, int NW>
+__global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 64 ? 2 : 1))) void attn_bwd_fused_bf16(AttnArgs a) {
+  static_assert(NW * 32 == KT, "one 32-row block per wave covers the tile");
+  constexpr int TP = KT * (DH + 8), PP = KT + 8;
+  static_assert(2 * TP >= KT * PP, "P fits in the K/V tile space");
+  __shared__ __attribute__((aligned(16))) bf16 sQ[TP];
+  __shared__ __attribute__((aligned(16))) bf16 sdO[TP];
+  __shared__ __attribute__((aligned(16))) bf16 sKV[2 * TP];  // K, V; later P, then dS ([query][key], pitch PP)
+  bf16* sK = sKV;
+  bf16* sV = sKV + TP;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
+  const int bh = xcd_block(blockIdx.y, gridDim.y), b = bh / a.H, hd = bh % a.H, S = a.S;
+  const int d = a.H * DH;
+  const float2* rtab = a.rope_tab;
+  const float scale = rsqrtf((float)DH), sl2 = kLog2e * scale;
+  const bf16* qkv = static_cast<const bf16*>(a.qkv);
+  const bf16* dO = static_cast<const bf16*>(a.dout);
+
+  // Q, dO, K, V tiles (rows >= S zero); RoPE on Q and K
+  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sdO, b, S, 0, rtab);
+  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S, 0,
+                              rtab);
+
+  // this lane's query: its D = rowsum(dO * O) and LSE
+  const int q = wave * 32 + l32;
+  const bool qv = q < S;
+  const long qrow = (long)(b * S + (qv ? q : 0));
+  float dsum = 0.f;
+  {
+    const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
+    const bf16* drow = dO + qrow * a.ld_do + hd * DH;
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) {
+      float ov[8], dv[8];
+      if (qv) {
+        unpack_frag(ld_frag(orow + 16 * s + 8 * half), ov);
+        unpack_frag(ld_frag(drow + 16 * s + 8 * half), dv);
+      } else {
+#pragma unroll
+        for (int v = 0; v < 8; ++v) ov[v] = dv[v] = 0.f;
+      }
+#pragma unroll
+      for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
+    }
+    dsum += __shfl_xor(dsum, 32, 64);
+  }
+  const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
+  __syncthreads();
+
+  // ---- scores, P, dS and dQ (lane = query)
+  const bool full = !CAUSAL && S == KT;
+  bf16x8 pk[KT / 32][2], sk[KT / 32][2];
+  {
+    f32x16 dq[DH / 32];
+#pragma unroll
+    for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) dq[i][r] = 0.f;
+#pragma unroll
+    for (int kb = 0; kb < KT / 32; ++kb) {
+      f32x16 st, dp;
+#pragma unroll
+      for (int r = 0; r < 16; ++r) st[r] = dp[r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < DH / 16; ++s) {
+        const bf16x8 qf = ld_frag(sQ + q * (DH + 8) + 16 * s + 8 * half);
+        const bf16x8 df = ld_frag(sdO + q * (DH + 8) + 16 * s + 8 * half);
+        st = mfma32(ld_frag(sK + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), qf, st);
+        dp = mfma32(ld_frag(sV + (kb * 32 + l32) * (DH + 8) + 16 * s + 8 * half), df, dp);
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int key = kb * 32 + perm_pos(r, half);
+        const bool ok = full || (qv && key < S && (!CAUSAL || key <= q));
+        const float p = ok ? __builtin_amdgcn_exp2f(fmaf(st[r], sl2, -lse)) : 0.f;
+        st[r] = p;
+        dp[r] = p * (dp[r] - dsum);  // dS
+      }
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        pk[kb][j] = pack8(st, j);
+        sk[kb][j] = pack8(dp, j);
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db) dq[db] = mfma32(perm_frag<DH>(sK, db, kb, j, lane), sk[kb][j], dq[db]);
+      }
+    }
+    if (qv) {
+      bf16* dst = static_cast<bf16*>(a.dqkv) + (long)(b * S + q) * a.ld_dqkv + hd * DH;
+      store_rows<DH>(dq, scale, a.rope, q, rtab, half, dst);
+    }
+  }
+
+  // a [query][key] block from the packed registers: register values 8j..8j+7
+  // of key block kb are keys kb*32 + 16j + 4*half + {0..3, 8..11}
+  auto put = [&](bf16x8 (&v)[KT / 32][2]) {
+#pragma unroll
+    for (int kb = 0; kb < KT / 32; ++kb)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const uint4 w = __builtin_bit_cast(uint4, v[kb][j]);
+        bf16* row = sKV + q * PP + kb * 32 + 16 * j + 4 * half;
+        *reinterpret_cast<uint2*>(row) = make_uint2(w.x, w.y);
+        *reinterpret_cast<uint2*>(row + 8) = make_uint2(w.z, w.w);
+      }
+  };
+  // dX[key][dim] += sum_q M[q][key] X[q][dim] over the whole tile (lane = key)
+  auto tmul = [&](const bf16* sX, f32x16 (&acc)[DH / 32]) {
+#pragma unroll
+    for (int i = 0; i < DH / 32; ++i)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][r] = 0.f;
+#pragma unroll
+    for (int qb = 0; qb < KT / 32; ++qb)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const bf16x8 mf = perm_frag<KT>(sKV, wave, qb, j, lane);
+#pragma unroll
+        for (int db = 0; db < DH / 32; ++db) acc[db] = mfma32(perm_frag<DH>(sX, db, qb, j, lane), mf, acc[db]);
+      }
+  };
+  const int key = wave * 32 + l32;
+  const bool kv = key < S;
+  bf16* kdst = static_cast<bf16*>(a.dqkv) + (long)(b * S + (kv ? key : 0)) * a.ld_dqkv;
+
+  __syncthreads();  // every wave is done with K and V
+  put(pk);
+  __syncthreads();
+  {
+    f32x16 dv[DH / 32];
+    tmul(sdO, dv);
+    if (kv) store_rows<DH>(dv, 1.f, false, key, nullptr, half, kdst + 2 * d + hd * DH);
+  }
+  __syncthreads();  // every wave is done with P
+  put(sk);
+  __syncthreads();
+  {
+    f32x16 dk[DH / 32];
+    tmul(sQ, dk);
+    if (kv) store_rows<DH>(dk, scale, a.rope, key, rtab, half, kdst + d + hd * DH);
+  }
+}
+
 // ================================================================ fp32 (small stages)
 // One workgroup per (batch, head), one thread per query (forward, dQ) or key
 // (dK, dV); head dim <= 128.
@@ -573,6 +724,11 @@ static hipError_t fwd_dh(const AttnArgs& a, hipStream_t s) {
 template <int DH>
 static hipError_t bwd_dh(const AttnArgs& a, hipStream_t s) {
   dim3 grid((a.S + 32 * ATT_NW - 1) / (32 * ATT_NW), a.B * a.H), block(64 * ATT_NW);
+  if (a.S <= KT) {  // one tile: the fused single-pass backward
+    if (a.causal) RG_LAUNCH((attn_bwd_fused_bf16<DH, true, ATT_NW>), dim3(1, a.B * a.H), block, 0, s, a);
+    else RG_LAUNCH((attn_bwd_fused_bf16<DH, false, ATT_NW>), dim3(1, a.B * a.H), block, 0, s, a);
+    return hipGetLastError();
+  }
   if (a.causal) {
     RG_LAUNCH((attn_bwd_dq_bf16<DH, true, ATT_NW>), grid, block, 0, s, a);
     RG_LAUNCH((attn_bwd_dkdv_bf16<DH, true, ATT_NW>), grid, block, 0, s, a);
