@@ -228,9 +228,10 @@ ringada_status ringada_loss_mse(void* stream, int32_t dtype, const void* y,
 /* Linear head on position 0 of each sequence + softmax cross-entropy, mean
  * over the batch.  y, dy: [batch, seq, d] in `dtype` (dy is fully written:
  * zero except position 0); w_h [d, n_classes] and b_h [n_classes] fp32;
- * labels [batch] int32 in [0, n_classes); g_wh, g_bh fp32 gradients are ADDED
- * into; loss is one device float, overwritten (may be NULL).
- * n_classes <= 16. */
+ * labels [batch] int32 in [0, n_classes); the fp32 gradients g_wh, g_bh and
+ * the mean loss (one device float, may be NULL) are ADDED into: zero them
+ * before the first call of an accumulation.  n_classes <= 16; d a multiple of
+ * 8; y, dy and w_h 16-B aligned. */
 ringada_status ringada_head_ce(void* stream, int32_t dtype, const void* y,
                                int32_t batch, int32_t seq, int32_t d,
                                const float* w_h, const float* b_h,

@@ -390,119 +390,113 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
 // logits and dlogits, (2) one thread per feature i accumulates gwh[i, :] over
 // the chunk and writes dy[b, 0, i].  It alone owns gwh / gbh / loss, so no
 // atomics are needed.  The other workgroups zero dy at positions 1..S-1.
-constexpr int HEAD_C = 16;      // maximum number of classes
-constexpr int HEAD_CHUNK = 64;  // maximum samples per LDS chunk
-constexpr int HEAD_NT = 1024;   // threads per workgroup (16 waves: the head does one sample per wave)
+constexpr int HEAD_C = 16;   // maximum number of classes
+constexpr int HEAD_SPW = 4;  // samples per workgroup (one wave each)
+// Workgroups 0 .. ceil(B / HEAD_SPW) - 1: one wave per sample for the logits,
+// the softmax and the loss, then one thread per feature for the sample's dY
+// row and its share of the W_h gradient (fp32 atomics: the gradients and the
+// loss are sums over the batch, added into the caller's buffers).  The other
+// workgroups zero rows 1..S-1 of every sequence with 16-B stores.
 template <typename T, int CN>  // CN: class count bound, compile time (the loops over classes unroll)
-__global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
-                                                 const float* bh, int C, const int* labels, T* dy,
-                                                 float* gwh, float* gbh, float* loss, int chunk) {
-  if (blockIdx.x > 0) {
-    const int nz = gridDim.x - 1;
+__global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh, const float* bh,
+                                                 int C, const int* labels, T* dy, float* gwh, float* gbh,
+                                                 float* loss) {
+  const int nce = (B + HEAD_SPW - 1) / HEAD_SPW;
+  if ((int)blockIdx.x >= nce) {
+    const int nz = gridDim.x - nce, z = blockIdx.x - nce;
     const int vpr = d * (int)sizeof(T) / 16;  // 16-B vectors per row
-    for (int r = blockIdx.x - 1; r < B * S; r += nz) {
-      if (r % S == 0) continue;
-      uint4* row = reinterpret_cast<uint4*>(dy + (long)r * d);
-      for (int i = threadIdx.x; i < vpr; i += HEAD_NT) row[i] = make_uint4(0, 0, 0, 0);
+    const long nvec = (long)B * (S - 1) * vpr;
+    for (long v = (long)z * 256 + threadIdx.x; v < nvec; v += (long)nz * 256) {
+      const long rr = v / vpr;
+      const long r = (rr / (S - 1)) * S + 1 + rr % (S - 1);
+      reinterpret_cast<uint4*>(dy + r * d)[v % vpr] = make_uint4(0, 0, 0, 0);
     }
     return;
   }
-  __shared__ float sdl[HEAD_CHUNK][CN];
-  __shared__ float sloss[HEAD_CHUNK];
-  __shared__ float sbh[CN];
-  __shared__ int slab[HEAD_CHUNK];
-  extern __shared__ __attribute__((aligned(16))) unsigned char head_smem[];
-  float* sW = reinterpret_cast<float*>(head_smem);                              // [d][C]
-  T* sY = reinterpret_cast<T*>(head_smem + ((size_t)d * C * 4 + 15) / 16 * 16);  // [chunk][d]
+  static_assert(HEAD_SPW * 64 == 256, "one wave per sample of the workgroup");
+  __shared__ float sdl[HEAD_SPW][CN];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  for (int i = threadIdx.x; i < d * C; i += HEAD_NT) sW[i] = wh[i];
-  if (threadIdx.x < C) sbh[threadIdx.x] = bh[threadIdx.x];
-  float total = 0.f;     // thread 0's running loss
-  float gb[CN];      // thread 0's running bias gradient
+  const int j0 = blockIdx.x * HEAD_SPW, j = j0 + wave;
+  if (j < B) {
+    // label and bias first, then the row in 8-feature chunks (16-B loads of y,
+    // 8 x C floats of W_h per chunk): few memory round trips in flight at once
+    const int lab = labels[j];
+    float bias[CN];
 #pragma unroll
-  for (int c = 0; c < CN; ++c) gb[c] = 0.f;
-  const int vpr = d * (int)sizeof(T) / 16;
-  for (int b0 = 0; b0 < B; b0 += chunk) {
-    const int nb = min(chunk, B - b0);
-    // the chunk's [CLS] rows -> LDS, 16 B per load
-    if (threadIdx.x < nb) slab[threadIdx.x] = labels[b0 + threadIdx.x];
-#pragma unroll 4
-    for (int v = threadIdx.x; v < nb * vpr; v += HEAD_NT) {
-      const int j = v / vpr, k = v % vpr;
-      reinterpret_cast<uint4*>(sY + (long)j * d)[k] = reinterpret_cast<const uint4*>(y + (long)(b0 + j) * S * d)[k];
+    for (int c = 0; c < CN; ++c) bias[c] = c < C ? bh[c] : 0.f;
+    const T* yr = y + (long)j * S * d;
+    float lg[CN];
+#pragma unroll
+    for (int c = 0; c < CN; ++c) lg[c] = 0.f;
+#pragma unroll 2
+    for (int v = lane; v < d / 8; v += 64) {
+      float yv[8];
+      if constexpr (std::is_same_v<T, bf16>) {
+        unpack_frag(ld_frag(yr + 8 * v), yv);
+      } else {
+        const float4 a = reinterpret_cast<const float4*>(yr)[2 * v], b = reinterpret_cast<const float4*>(yr)[2 * v + 1];
+        yv[0] = a.x; yv[1] = a.y; yv[2] = a.z; yv[3] = a.w; yv[4] = b.x; yv[5] = b.y; yv[6] = b.z; yv[7] = b.w;
+      }
+      const float* wr = wh + (long)8 * v * C;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+#pragma unroll
+        for (int c = 0; c < CN; ++c)
+          if (c < C) lg[c] += yv[e] * wr[e * C + c];
     }
-    __syncthreads();
-    // phase 1: logits and dlogits, one wave per sample
-    for (int j = wave; j < nb; j += HEAD_NT / 64) {
-      float lg[CN];
-#pragma unroll
-      for (int c = 0; c < CN; ++c) lg[c] = 0.f;
-      for (int i = lane; i < d; i += 64) {
-        const float yi = St<T>::ld(sY, (long)j * d + i);
-#pragma unroll
-        for (int c = 0; c < CN; ++c)
-          if (c < C) lg[c] += yi * sW[i * C + c];
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int c = 0; c < CN; ++c)
-        if (c < C) {
-          lg[c] = wave_sum(lg[c]) + sbh[c];
-          mx = fmaxf(mx, lg[c]);
-        }
-      float se = 0.f, ll = 0.f;
-      const int lab = slab[j];
-#pragma unroll
-      for (int c = 0; c < CN; ++c)
-        if (c < C) {
-          se += __expf(lg[c] - mx);
-          if (c == lab) ll = lg[c];
-        }
-      if (lane == 0) {
-        sloss[j] = -(ll - mx - __logf(se));
-#pragma unroll
-        for (int c = 0; c < CN; ++c)
-          if (c < C) sdl[j][c] = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
-      }
-    }
-    __syncthreads();
-    // phase 2: one thread per feature
-    for (int i = threadIdx.x; i < d; i += HEAD_NT) {
-      float w[CN], acc[CN];
-#pragma unroll
-      for (int c = 0; c < CN; ++c) {
-        w[c] = c < C ? sW[i * C + c] : 0.f;
-        acc[c] = 0.f;
-      }
-      for (int j = 0; j < nb; ++j) {
-        const float yi = St<T>::ld(sY, (long)j * d + i);
-        float g = 0.f;
-#pragma unroll
-        for (int c = 0; c < CN; ++c)
-          if (c < C) {
-            acc[c] += yi * sdl[j][c];
-            g += sdl[j][c] * w[c];
-          }
-        St<T>::st(dy, (long)(b0 + j) * S * d + i, g);
-      }
-#pragma unroll
-      for (int c = 0; c < CN; ++c)
-        if (c < C) gwh[(long)i * C + c] += acc[c];
-    }
-    if (threadIdx.x == 0)
-      for (int j = 0; j < nb; ++j) {
-        total += sloss[j];
-#pragma unroll
-        for (int c = 0; c < CN; ++c)
-          if (c < C) gb[c] += sdl[j][c];
-      }
-    __syncthreads();
-  }
-  if (threadIdx.x == 0) {
+    float mx = -INFINITY;
 #pragma unroll
     for (int c = 0; c < CN; ++c)
-      if (c < C) gbh[c] += gb[c];
-    if (loss) *loss = total / (float)B;
+      if (c < C) {
+        lg[c] = wave_sum(lg[c]) + bias[c];
+        mx = fmaxf(mx, lg[c]);
+      }
+    float se = 0.f, ll = 0.f;
+#pragma unroll
+    for (int c = 0; c < CN; ++c)
+      if (c < C) {
+        se += __expf(lg[c] - mx);
+        if (c == lab) ll = lg[c];
+      }
+    if (lane == 0) {
+      if (loss) unsafeAtomicAdd(loss, -(ll - mx - __logf(se)) / (float)B);
+#pragma unroll
+      for (int c = 0; c < CN; ++c)
+        if (c < C) {
+          const float g = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
+          sdl[wave][c] = g;
+          unsafeAtomicAdd(gbh + c, g);
+        }
+    }
+  } else if (lane < CN) {
+    sdl[wave][lane] = 0.f;
+  }
+  __syncthreads();
+  const int ns = min(HEAD_SPW, B - j0);
+  for (int i = threadIdx.x; i < d; i += 256) {
+    float w[CN], acc[CN], yi[HEAD_SPW];
+#pragma unroll
+    for (int c = 0; c < CN; ++c) {
+      w[c] = c < C ? wh[(long)i * C + c] : 0.f;
+      acc[c] = 0.f;
+    }
+#pragma unroll
+    for (int s = 0; s < HEAD_SPW; ++s) yi[s] = s < ns ? St<T>::ld(y, (long)(j0 + s) * S * d + i) : 0.f;
+#pragma unroll
+    for (int s = 0; s < HEAD_SPW; ++s) {
+      if (s >= ns) break;
+      float g = 0.f;
+#pragma unroll
+      for (int c = 0; c < CN; ++c)
+        if (c < C) {
+          acc[c] += yi[s] * sdl[s][c];
+          g += sdl[s][c] * w[c];
+        }
+      St<T>::st(dy, (long)(j0 + s) * S * d + i, g);
+    }
+#pragma unroll
+    for (int c = 0; c < CN; ++c)
+      if (c < C) unsafeAtomicAdd(gwh + (long)i * C + c, acc[c]);
   }
 }
 
@@ -512,32 +506,28 @@ hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const f
   if (!y || !wh || !bh || !labels || !dy || !gwh || !gbh || B <= 0 || S <= 0 || d <= 0 || C < 1 || C > HEAD_C)
     return hipErrorInvalidValue;
   const size_t es = dtype == DT_BF16 ? 2 : 4;
-  // rows move as 16-B vectors: rows a multiple of 16 B, y and dy 16-B aligned
-  if ((d * es) % 16 || (reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(dy)) & 15u)
+  // rows move as 16-B vectors: d a multiple of 8, y, dy and w_h 16-B aligned
+  if (d % 8 || (d * es) % 16 ||
+      (reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(wh)) & 15u)
     return hipErrorInvalidValue;
-  const long zero_rows = (long)B * (S - 1);
-  const dim3 grid(1 + (unsigned)(zero_rows < 256 ? zero_rows : 256)), block(HEAD_NT);
-  // LDS: W_h (d x C floats) and the chunk's rows, within 64 KiB together
-  // with the kernel's static arrays (dlogits, losses, labels of a chunk; bias)
-  const size_t budget = 65536 - sizeof(float) * (HEAD_CHUNK * (HEAD_C + 2) + HEAD_C);
-  const size_t wbytes = ((size_t)d * C * 4 + 15) / 16 * 16;
-  if (wbytes + es * d > budget) return hipErrorInvalidValue;
-  const int chunk = (int)std::min<size_t>(HEAD_CHUNK, (budget - wbytes) / (es * (size_t)d));
-  const size_t sh = wbytes + (size_t)chunk * d * es;
+  const int nce = (B + HEAD_SPW - 1) / HEAD_SPW;
+  const long nvec = (long)B * (S - 1) * (long)(d * es / 16);
+  const int nz = (int)std::min<long>(256, (nvec + 255) / 256);
+  const dim3 grid(nce + nz), block(256);
   if (dtype == DT_BF16) {
     if (C == 2)
-      RG_LAUNCH((head_ce_k<bf16, 2>), grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels, (bf16*)dy,
-                gwh, gbh, loss, chunk);
+      RG_LAUNCH((head_ce_k<bf16, 2>), grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels, (bf16*)dy,
+                gwh, gbh, loss);
     else
-      RG_LAUNCH((head_ce_k<bf16, HEAD_C>), grid, block, sh, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
-                (bf16*)dy, gwh, gbh, loss, chunk);
+      RG_LAUNCH((head_ce_k<bf16, HEAD_C>), grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels,
+                (bf16*)dy, gwh, gbh, loss);
   } else {
     if (C == 2)
-      RG_LAUNCH((head_ce_k<float, 2>), grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels, (float*)dy,
-                gwh, gbh, loss, chunk);
+      RG_LAUNCH((head_ce_k<float, 2>), grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels, (float*)dy,
+                gwh, gbh, loss);
     else
-      RG_LAUNCH((head_ce_k<float, HEAD_C>), grid, block, sh, s, (const float*)y, B, S, d, wh, bh, C, labels,
-                (float*)dy, gwh, gbh, loss, chunk);
+      RG_LAUNCH((head_ce_k<float, HEAD_C>), grid, block, 0, s, (const float*)y, B, S, d, wh, bh, C, labels,
+                (float*)dy, gwh, gbh, loss);
   }
   return hipGetLastError();
 }
