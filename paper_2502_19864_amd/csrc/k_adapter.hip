@@ -189,7 +189,11 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   }
 }
 
-// ================================================================ bf16 backward
+// ================================================================ bf16 backward, d <= 1024
+// One workgroup of 16 waves per 16 tokens: the norm backward (row sums over
+// the waves through LDS), dV = dZ W_up^T (k split over 4 waves), dU = dV *
+// gelu'(U), and dzin = dZ + dU W_down^T, with every weight fragment loaded
+// while the previous phase runs.
 template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int KS = NW / 4;
@@ -221,11 +225,10 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   // fragments of W_up for the first contraction: in flight during the norm backward
   const int ug = wave % 4, ks = wave / 4;
   constexpr int NSTEP = SLICE / 32;
-  constexpr bool PRE = FB <= 4;  // early loads while the registers allow
-  constexpr int NPRE = PRE ? NSTEP : 1;
+  static_assert(FB <= 4, "d <= 1024: every weight fragment fits the registers (wider widths split the work)");
   const bool has_ad = a.wup != nullptr;  // else: the norm backward only
-  bf16x8 wup_f[NPRE];
-  if constexpr (PRE) {
+  bf16x8 wup_f[NSTEP];
+  {
     if (has_ad) {
 #pragma unroll
       for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
@@ -289,7 +292,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   if (!has_ad) return;
   // W_down fragments of the last contraction, in flight during the dV one
   bf16x8 w0[FB], w1[FB];
-  if (PRE && a.dzin) {
+  if (a.dzin) {
 #pragma unroll
     for (int b = 0; b < FB; ++b) {
       w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
@@ -305,20 +308,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     const float uu[4] = {__uint_as_float(uraw.x << 16), __uint_as_float(uraw.x & 0xffff0000u),
                          __uint_as_float(uraw.y << 16), __uint_as_float(uraw.y & 0xffff0000u)};
     f32x4 dv = {0.f, 0.f, 0.f, 0.f};
-    if constexpr (PRE) {
 #pragma unroll
-      for (int j = 0; j < NSTEP; ++j) dv = mfma16(wup_f[j], ld_frag(zr + j * 32), dv);
-    } else {
-      constexpr int RUN = NSTEP < 8 ? NSTEP : 8;
-#pragma unroll
-      for (int k0 = 0; k0 < NSTEP; k0 += RUN) {
-        bf16x8 w[RUN];
-#pragma unroll
-        for (int j = 0; j < RUN; ++j) w[j] = ld_frag(pack_a_frag(a.wup, D, wave, k0 + j, lane));
-#pragma unroll
-        for (int j = 0; j < RUN; ++j) dv = mfma16(w[j], ld_frag(zr + (k0 + j) * 32), dv);
-      }
-    }
+    for (int j = 0; j < NSTEP; ++j) dv = mfma16(wup_f[j], ld_frag(zr + j * 32), dv);
     if constexpr (KS > 1) {
 #pragma unroll
       for (int r = 0; r < 4; ++r) sPart[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = dv[r];
@@ -346,13 +337,6 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 
   // ---- dzin^T[f][token] = dZ + W_down[f][:] . dU[token][:]
   const bf16x8 u0 = ld_frag(sdU + l16 * GP + 8 * grp), u1 = ld_frag(sdU + l16 * GP + 32 + 8 * grp);
-  if constexpr (!PRE) {
-#pragma unroll
-    for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
-      w1[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 1, lane));
-    }
-  }
 #pragma unroll
   for (int b = 0; b < FB; ++b) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};

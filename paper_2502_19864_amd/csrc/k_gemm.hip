@@ -12,6 +12,8 @@
 // f32: a plain FMA tile kernel (used by the small fp32 stage only).
 #include <type_traits>
 
+#include <utility>
+
 #include "common.h"
 #include "kernels.h"
 
@@ -293,6 +295,18 @@ __device__ __forceinline__ void tile_coords(int M, int N, int& m0, int& n0) {
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
+// Scheduling hint for one k-step of the pipelined kernel: alternate one LDS
+// fragment read (of the next k-step) with one MFMA (of this one), ND reads in
+// all, so the reads drain while the matrix core works instead of bunching up
+// in front of it (1-3 % on every tile shape measured).
+template <int ND, int... Q>
+__device__ __forceinline__ void interleave_ds_mfma(std::integer_sequence<int, Q...>) {
+  ([] {
+    if constexpr (Q < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
+  }(), ...);
+}
+
 // Global -> LDS DMA, 16 B per lane (lane i lands at the LDS address + 16 i),
 // issued from inline assembly: scalar base + 32-bit per-lane byte
 // offset, LDS destination (wave-uniform byte address) in M0.  The compiler's
@@ -456,6 +470,7 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
         read_frags(stage_base(std::integral_constant<int, sn>{}), 0, 0);
       }
       mfmas(ks & 1);
+      interleave_ds_mfma<FM + FN>(std::make_integer_sequence<int, FM * FN>{});
     }
   };
   for (int kt = 0; kt < nk; kt += NS) {
