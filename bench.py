@@ -77,30 +77,43 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def _f64(v):
+    """float64 copies of every array in a nest of lists, tuples and dicts."""
+    if isinstance(v, dict):
+        return {k: _f64(x) for k, x in v.items()}
+    if isinstance(v, (list, tuple)):
+        return type(v)(_f64(x) for x in v)
+    if isinstance(v, np.ndarray) and v.dtype.kind == "f":
+        return v.astype(np.float64)
+    return v
+
+
 def cpu_baseline(w, inp):
-    """The float oracle timed on this host: one full step (forward, head loss,
-    early-stopped backward, SGD) on every sample of the workload, fp32."""
+    """The oracle as the tests run it (numpy, float64) timed on this host: one
+    full step (forward, head loss, early-stopped backward, SGD) on every
+    sample of the workload."""
     import oracle as O
     from threadpoolctl import threadpool_info
     from paper_2502_19864_amd.workloads import adapters_as_computed
     desc = O.make_desc(w.arch, w.n_blocks, w.d_model, w.n_heads, w.d_ffn, w.d_adapter, placement=w.placement)
-    W = inp["weights"]
-    A = adapters_as_computed(w, inp["adapters"])
+    W = _f64(inp["weights"])
+    A = _f64(adapters_as_computed(w, inp["adapters"]))
+    x = _f64(inp["x"])
     t0 = time.perf_counter()
-    y, caches = O.stage_forward(desc, W, A, inp["x"])
+    y, caches = O.stage_forward(desc, W, A, x)
     if w.loss == "cls_ce":
-        _, dy, _, _ = O.cls_head_ce(y, inp["w_h"], inp["b_h"], inp["labels"])
+        _, dy, _, _ = O.cls_head_ce(y, _f64(inp["w_h"]), _f64(inp["b_h"]), inp["labels"])
     elif w.loss == "mse":
-        _, dy = O.mse_loss(y, inp["target"])
+        _, dy = O.mse_loss(y, _f64(inp["target"]))
     else:
-        dy = inp["dy"]
+        dy = _f64(inp["dy"])
     _, grads = O.stage_backward(desc, W, A, caches, dy, w.lowest_unfrozen)
     O.sgd_step(A, grads, 1e-3)
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     return {"value": round(w.batch / dt, 3), "unit": "samples/s", "cores": int(threads), "kind": "oracle",
             "sample": f"one full step (forward, head loss, backward to block {w.lowest_unfrozen}, SGD) of "
-                      f"the {w.name} workload, all {w.batch} samples, numpy float32 oracle, {dt:.2f} s"}
+                      f"the {w.name} workload, all {w.batch} samples, numpy float64 oracle, {dt:.2f} s"}
 
 
 def main():
