@@ -591,6 +591,10 @@ __device__ __forceinline__ void gemm_f32_body(const GemmArgs& a) {
   __global__ __launch_bounds__(256) void NAME##_pipe(GemmArgs a) {                   \
     gemm_bf16_pipe_body<BM, BN, WM, WN, 64, NS, E, 4>(a);                            \
   }                                                                                  \
+  template <int BM, int BN, int WM, int WN, int NS, Epi E>                           \
+  __global__ __launch_bounds__(512) void NAME##_pipe8(GemmArgs a) {                  \
+    gemm_bf16_pipe_body<BM, BN, WM, WN, 64, NS, E, 4>(a);                            \
+  }                                                                                  \
   template <Epi E>                                                                   \
   __global__ __launch_bounds__(256) void NAME##_f32(GemmArgs a) {                    \
     gemm_f32_body<E>(a);                                                             \
@@ -623,12 +627,20 @@ static constexpr bool role_has(Role r, Epi e) {
 }
 
 // Tile shapes of the pipelined kernel (BK = 64), chosen per GEMM shape by
-// measurement on the BERT-base stage: 128x192 (2x2 waves of 64x96) for wide
-// outputs with short K, 128x96 (4x1 waves of 32x96, three stages) for
-// 768-wide outputs, 128x128 (2x2 waves of 64x64) otherwise and for the
-// SwiGLU epilogue, which needs gate/up block pairs in one wave.  The register
-// staged kernel covers K % 64 != 0 and unaligned epilogue operands.
-enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_REG_128x128, C_REG_64x128 };
+// measurement on the BERT-base, BERT-large and LLaMA-7B stage shapes:
+//  - 128x192 (2x2 waves of 64x96, two stages) for wide outputs with K <= 1024;
+//  - 128x96 (4x1 waves of 32x96, three stages) for outputs up to 1024 wide
+//    that 96 divides;
+//  - for K > 1024, 256x192 (8 waves of 64x96, two stages) or 256x128 (8
+//    waves of 64x64, three stages: one workgroup per CU either way, and the
+//    third stage hides the HBM latency of weights that no cache holds, 10-17%
+//    on the LLaMA-7B shapes) when that still gives every CU a tile;
+//  - 128x128 (2x2 waves of 64x64) otherwise and for the SwiGLU epilogues,
+//    which need gate/up block pairs in one wave: two stages (two workgroups
+//    per CU) from two tiles per CU on, three stages below.
+// The register staged kernel covers K % 64 != 0 and unaligned epilogue operands.
+enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_P256x192_8W, C_P256x128_8W, C_REG_128x128,
+           C_REG_64x128 };
 
 template <Role R, Epi E>
 static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t s) {
@@ -667,6 +679,14 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       break;                                                                                             \
     case C_P128x128_3:                                                                                   \
       RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
+      break;                                                                                             \
+    case C_P256x192_8W:                                                                                  \
+      if constexpr (E != Epi::SwiGlu)                                                                    \
+        RG_LAUNCH((NAME##_pipe8<256, 192, 4, 2, 2, E>), RG_TILES(256, 192), dim3(512), 0, s, a);          \
+      break;                                                                                             \
+    case C_P256x128_8W:                                                                                  \
+      if constexpr (E != Epi::SwiGlu)                                                                    \
+        RG_LAUNCH((NAME##_pipe8<256, 128, 4, 2, 3, E>), RG_TILES(256, 128), dim3(512), 0, s, a);          \
       break;                                                                                             \
     case C_REG_128x128:                                                                                  \
       RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
@@ -731,12 +751,16 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
                         (!a.out2 || (al16(a.out2) && a.ldo2 % 8 == 0)) && a.half % 8 == 0;
     const bool small_off = ((double)(a.M - 1) * a.lda + a.K) * 2 < 4294967296.0 &&
                            ((double)(a.N - 1) * a.ldb + a.K) * 2 < 4294967296.0;
-    const long t192 = (long)((a.M + 127) / 128) * ((a.N + 191) / 192);
+    auto tiles = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
+    // two stages (two workgroups per CU) once there are two 128x128 tiles per CU
+    const Cfg c128 = tiles(128, 128) >= 512 ? C_P128x128_2 : C_P128x128_3;
     if (a.K % 64 == 0 && al_epi && small_off) {
-      if (epi == Epi::SwiGlu || epi == Epi::DSwiGlu) cfg = a.K <= 1024 ? C_P128x128_2 : C_P128x128_3;
-      else if (a.N % 192 == 0 && a.K <= 1024 && t192 >= 256) cfg = C_P128x192;
+      if (epi == Epi::SwiGlu || epi == Epi::DSwiGlu) cfg = c128;
+      else if (a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
       else if (a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
-      else cfg = a.K <= 1024 ? C_P128x128_2 : C_P128x128_3;
+      else if (a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
+      else if (a.K > 1024 && a.N % 128 == 0 && tiles(256, 128) >= 256) cfg = C_P256x128_8W;
+      else cfg = c128;
     } else {
       const long tiles128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
       cfg = tiles128 >= 512 ? C_REG_128x128 : C_REG_64x128;
