@@ -635,9 +635,10 @@ static constexpr bool role_has(Role r, Epi e) {
 //    waves of 64x64, three stages: one workgroup per CU either way, and the
 //    third stage hides the HBM latency of weights that no cache holds, 10-17%
 //    on the LLaMA-7B shapes) when that still gives every CU a tile;
-//  - 128x128 (2x2 waves of 64x64) otherwise and for the SwiGLU epilogues,
-//    which need gate/up block pairs in one wave: two stages (two workgroups
-//    per CU) from two tiles per CU on, three stages below.
+//  - 128x128 (2x2 waves of 64x64) otherwise: two stages (two workgroups per
+//    CU) from two tiles per CU on, three stages below.
+// The SwiGLU epilogues take only the 64-wide wave tiles (a gate/up block pair
+// per wave): 256x128 or 128x128.
 // The register staged kernel covers K % 64 != 0 and unaligned epilogue operands.
 enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_P256x192_8W, C_P256x128_8W, C_REG_128x128,
            C_REG_64x128 };
@@ -685,8 +686,7 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
         RG_LAUNCH((NAME##_pipe8<256, 192, 4, 2, 2, E>), RG_TILES(256, 192), dim3(512), 0, s, a);          \
       break;                                                                                             \
     case C_P256x128_8W:                                                                                  \
-      if constexpr (E != Epi::SwiGlu)                                                                    \
-        RG_LAUNCH((NAME##_pipe8<256, 128, 4, 2, 3, E>), RG_TILES(256, 128), dim3(512), 0, s, a);          \
+      RG_LAUNCH((NAME##_pipe8<256, 128, 4, 2, 3, E>), RG_TILES(256, 128), dim3(512), 0, s, a);            \
       break;                                                                                             \
     case C_REG_128x128:                                                                                  \
       RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
@@ -755,10 +755,10 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     // two stages (two workgroups per CU) once there are two 128x128 tiles per CU
     const Cfg c128 = tiles(128, 128) >= 512 ? C_P128x128_2 : C_P128x128_3;
     if (a.K % 64 == 0 && al_epi && small_off) {
-      if (epi == Epi::SwiGlu || epi == Epi::DSwiGlu) cfg = c128;
-      else if (a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
-      else if (a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
-      else if (a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
+      const bool glu = epi == Epi::SwiGlu || epi == Epi::DSwiGlu;
+      if (!glu && a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
+      else if (!glu && a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
+      else if (!glu && a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
       else if (a.K > 1024 && a.N % 128 == 0 && tiles(256, 128) >= 256) cfg = C_P256x128_8W;
       else cfg = c128;
     } else {

@@ -137,14 +137,15 @@ def floor_bound(floor, key):
     return max(2e-2, 2.0 * floor[key])
 
 
-def llama_floor(w, inp, c, dy, batch, seq):
+def llama_floor(w, inp, c, dy, batch, seq, rows=None):
     """Per-tensor deviation (max |.| / max |ref|) of the bf16-emulated run
-    from the oracle on x[:batch, :seq]: {'y': e, 'dx': e (c < 0),
-    (l, a, name): e}."""
+    from the oracle on x[:batch, :seq] (or on the samples listed in `rows`,
+    first seq positions): {'y': e, 'dx': e (c < 0), (l, a, name): e}."""
     desc = oracle_desc(w)
     W, A = to64(inp, w)
-    x = np.asarray(inp["x"], np.float64)[:batch, :seq]
-    dy = np.asarray(dy, np.float64)[:batch, :seq]
+    pick = slice(0, batch) if rows is None else list(rows)
+    x = np.asarray(inp["x"], np.float64)[pick, :seq]
+    dy = np.asarray(dy, np.float64)[pick, :seq]
     Bb, S, d = x.shape
     y_ref, c_ref = O.stage_forward(desc, W, A, x)
     dx_ref, g_ref = O.stage_backward(desc, W, A, c_ref, dy, c)

@@ -249,25 +249,28 @@ def test_bert_large_share_parity(torch):
 
 def test_llama_share_parity_on_a_causal_prefix(torch):
     """Full-size LLaMA share in the benchmark's launch configuration.  The
-    incoming gradient is zero outside sample 0's first 64 positions; with
-    causal attention and batch independence, outputs and gradients then equal
-    the oracle's on that prefix exactly.  Bound per tensor: max(2e-2, twice
-    the bf16 noise floor of that tensor), the floor being the oracle re-run
-    with the path's bf16 storage roundings (tests/bf16_floor.py)."""
+    incoming gradient is zero outside the first 64 positions of the first and
+    the last sample (token rows 0-63 and 1536-1599, in different GEMM row
+    tiles); with causal attention and batch independence, outputs and
+    gradients then equal the oracle's on those two prefixes exactly.  Bound
+    per tensor: max(2e-2, twice the bf16 noise floor of that tensor), the
+    floor being the oracle re-run with the path's bf16 storage roundings
+    (tests/bf16_floor.py)."""
     from bf16_floor import llama_floor
     w = WORKLOADS["llama7b_share"]
     inp = make_inputs(w)
     P = 64
+    rows = [0, w.batch - 1]
     dy = np.zeros_like(inp["dy"])
-    dy[0, :P] = inp["dy"][0, :P]
+    dy[rows, :P] = inp["dy"][rows, :P]
     st = Stage(w, inp)
     try:
         gpu = run_gpu(torch, st, w, inp, w.lowest_unfrozen, dy=dy)
     finally:
         st.close()
-    ref = oracle_run(w, inp, w.lowest_unfrozen, dy=dy, batch=1, seq=P)
-    floor = llama_floor(w, inp, w.lowest_unfrozen, dy, batch=1, seq=P)
-    errs = {"y": rel_err(gpu["y"][:1, :P], ref["y"])}
+    ref = oracle_run(w, inp, w.lowest_unfrozen, dy=dy[rows, :P], x=inp["x"][rows, :P])
+    floor = llama_floor(w, inp, w.lowest_unfrozen, dy, batch=None, seq=P, rows=rows)
+    errs = {"y": rel_err(gpu["y"][rows, :P], ref["y"])}
     for l in range(w.n_blocks):
         for a in range(2):
             for k in ("w_down", "w_up"):
