@@ -86,17 +86,19 @@ __device__ __forceinline__ void st8(bf16* p, const float v[8]) {
   *reinterpret_cast<bf16x8*>(p) = pack_frag(v);
 }
 
-// bf16 epilogue on eight consecutive output columns n..n+7 of row m
+// bf16 epilogue on eight consecutive output columns n..n+7 of row m; the
+// caller passes those columns' bias (Store, Gelu) as fp32, from LDS
 template <Epi E>
-__device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float v[8]) {
+__device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float v[8], const float* bias8,
+                                          const bf16x8* aux8) {
   const long r = m;
   bf16* out = static_cast<bf16*>(a.out);
   if constexpr (E == Epi::Store || E == Epi::Gelu) {
     if (a.bias) {
-      float b[8];
-      ld8(static_cast<const bf16*>(a.bias) + n, b);
-#pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] += b[i];
+      const float4 lo = *reinterpret_cast<const float4*>(bias8);
+      const float4 hi = *reinterpret_cast<const float4*>(bias8 + 4);
+      v[0] += lo.x; v[1] += lo.y; v[2] += lo.z; v[3] += lo.w;
+      v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
     }
     if constexpr (E == Epi::Gelu) {
       if (a.out2) st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + n, v);
@@ -106,20 +108,20 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float
     st8(out + r * a.ldo + n, v);
   } else if constexpr (E == Epi::Resid) {
     float x[8];
-    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, x);
+    unpack_frag(aux8[0], x);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += x[i];
     st8(out + r * a.ldo + n, v);
   } else if constexpr (E == Epi::DGelu) {
     float x[8];
-    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, x);
+    unpack_frag(aux8[0], x);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] *= gelu_grad_fast(x[i]);
     st8(out + r * a.ldo + n, v);
   } else if constexpr (E == Epi::DSwiGlu) {
     float g[8], u[8], dg[8], du[8];
-    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + n, g);
-    ld8(static_cast<const bf16*>(a.aux) + r * a.ld_aux + a.half + n, u);
+    unpack_frag(aux8[0], g);
+    unpack_frag(aux8[1], u);
 #pragma unroll
     for (int i = 0; i < 8; ++i) {
       const float sg = sigmoid_f(g[i]);
@@ -364,10 +366,15 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
   static_assert(E != Epi::SwiGlu || FN % 2 == 0, "SwiGlu needs gate/up block pairs");
   // output tile staging for the epilogue: fp32 rows of BN + 4 (the 16-B pad
   // spreads the rows one fragment store touches over all banks), RPP rows
-  // (a multiple of 32) per pass through the stage buffers
+  // (a multiple of 32)
+  // per pass through the stage buffers; the tile's bias columns (fp32) sit
+  // at the end of those buffers, past the staging rows
   constexpr int CPF = BN + 4;
-  constexpr int RPP = epi_rows(BM, CPF * 4, NS * STAGE);
-  static_assert(RPP >= 32 && BM % RPP == 0 && RPP * CPF * 4 <= NS * STAGE, "epilogue passes of whole 32-row blocks");
+  constexpr bool HAS_BIAS = E == Epi::Store || E == Epi::Gelu;
+  constexpr int BIASB = HAS_BIAS ? BN * 4 : 0;
+  constexpr int RPP = epi_rows(BM, CPF * 4, NS * STAGE - BIASB);
+  static_assert(RPP >= 32 && BM % RPP == 0 && RPP * CPF * 4 + BIASB <= NS * STAGE,
+                "epilogue passes of whole 32-row blocks");
   // the DMA is invisible to the compiler, so one array serves every stage
   __shared__ __attribute__((aligned(1024))) char smem[NS * STAGE];
   auto stage_base = [&](auto S) -> char* { return smem + decltype(S)::value * STAGE; };
@@ -379,6 +386,34 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
   const bf16* A = static_cast<const bf16*>(a.A);
   const bf16* B = static_cast<const bf16*>(a.B);
   const int M = a.M, N = a.N, K = a.K;
+  // the tile's bias, fetched now (eight columns per thread of the first BN/8)
+  // so that the epilogue finds it in LDS instead of waiting on global loads
+  bf16x8 bias_raw = {};
+  if constexpr (HAS_BIAS)
+    if (a.bias && tid < BN / 8 && n0 + tid * 8 < N)
+      bias_raw = *reinterpret_cast<const bf16x8*>(static_cast<const bf16*>(a.bias) + n0 + tid * 8);
+  // The epilogue's second operand (residual, pre-activation, gate/up) was
+  // written long before and sits in HBM; read all at once at the end of every
+  // tile it stalls the epilogue.  One dword from each of its 128-B lines,
+  // loaded now, streams it into the caches behind the main loop (the values
+  // are never used).  Row segments of BN columns touch at most PF_L lines.
+  constexpr bool HAS_AUX = E == Epi::Resid || E == Epi::DGelu || E == Epi::DSwiGlu;
+  constexpr int PF_L = (BN * 2 + 127) / 128 + 1, PF_SEG = E == Epi::DSwiGlu ? 2 : 1;
+  constexpr int PF_N = HAS_AUX ? (BM * PF_L * PF_SEG + NT - 1) / NT : 0;
+  uint32_t pf[PF_N > 0 ? PF_N : 1];
+  if constexpr (HAS_AUX) {
+    const int ncol = min(BN, N - n0);
+#pragma unroll
+    for (int i = 0; i < PF_N; ++i) {
+      const int idx = tid + i * NT;
+      if (idx < BM * PF_L * PF_SEG) {
+        const int seg = idx / (BM * PF_L), row = (idx / PF_L) % BM, line = idx % PF_L;
+        const long off = (long)min(m0 + row, M - 1) * a.ld_aux + n0 + seg * a.half;
+        const int byte = min(line * 128, ncol * 2 - 4);
+        pf[i] = *reinterpret_cast<const uint32_t*>(reinterpret_cast<const char*>(a.aux) + off * 2 + byte);
+      }
+    }
+  }
 
   // DMA: instruction i of this wave fills rows (i*NW + wave)*RPI .. +RPI-1;
   // lane -> row lane / CPR, LDS position lane % CPR.  Byte offsets from the
@@ -485,16 +520,44 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
   // elementwise work runs on eight-column chunks, on the fp32 sums, with one
   // rounding to bf16 at the store
   wait_vm_lgkm<0>();
+  if constexpr (HAS_AUX) {
+#pragma unroll
+    for (int i = 0; i < PF_N; ++i) asm volatile("" ::"v"(pf[i]));  // keeps the prefetch loads
+  }
   barrier();  // every wave is done reading operand tiles
   float* cf = reinterpret_cast<float*>(smem);
+  float* cbias = reinterpret_cast<float*>(smem + NS * STAGE - BIASB);
+  if constexpr (HAS_BIAS)
+    if (a.bias && tid < BN / 8) {
+      float f[8];
+      unpack_frag(bias_raw, f);
+      *reinterpret_cast<float4*>(cbias + tid * 8) = make_float4(f[0], f[1], f[2], f[3]);
+      *reinterpret_cast<float4*>(cbias + tid * 8 + 4) = make_float4(f[4], f[5], f[6], f[7]);
+    }
   auto ld_tile8 = [&](int row, int col, float v[8]) {
     const float4 lo = *reinterpret_cast<const float4*>(cf + row * CPF + col);
     const float4 hi = *reinterpret_cast<const float4*>(cf + row * CPF + col + 4);
     v[0] = lo.x; v[1] = lo.y; v[2] = lo.z; v[3] = lo.w;
     v[4] = hi.x; v[5] = hi.y; v[6] = hi.z; v[7] = hi.w;
   };
+  constexpr int CPRW8 = BN / 8, NCH8 = RPP * CPRW8;
 #pragma unroll
   for (int p = 0; p < BM / RPP; ++p) {
+    // this pass's second-operand chunks, all loads in flight before the
+    // staging so that their latency overlaps it
+    bf16x8 ax[HAS_AUX ? NCH8 / NT : 1][PF_SEG];
+    if constexpr (HAS_AUX) {
+#pragma unroll
+      for (int i = 0; i < NCH8 / NT; ++i) {
+        const int idx = tid + i * NT;
+        const int m = m0 + p * RPP + idx / CPRW8, n = n0 + (idx % CPRW8) * 8;
+        if (m < M && n < N) {
+          const bf16* x = static_cast<const bf16*>(a.aux) + (long)m * a.ld_aux + n;
+#pragma unroll
+          for (int sg = 0; sg < PF_SEG; ++sg) ax[i][sg] = *reinterpret_cast<const bf16x8*>(x + sg * a.half);
+        }
+      }
+    }
 #pragma unroll
     for (int i = 0; i < FM; ++i) {
       if ((wm * TM + i * 32) / RPP != p) continue;  // wave-uniform
@@ -523,17 +586,28 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
         ld_tile8(row, c + 32, uv);
         epilogue_swiglu8(a, m, (n0 + c) / 64 * 32 + (c % 64), gv, uv);
       }
-    } else {
-      constexpr int CPRW = BN / 8, NCH = RPP * CPRW;
-      static_assert(NCH % NT == 0, "whole passes");
-#pragma unroll 2
-      for (int idx = tid; idx < NCH; idx += NT) {
-        const int row = idx / CPRW, c = (idx % CPRW) * 8;
+    } else if constexpr (HAS_AUX) {
+      static_assert(NCH8 % NT == 0, "whole passes");
+#pragma unroll
+      for (int i = 0; i < NCH8 / NT; ++i) {
+        const int idx = tid + i * NT;
+        const int row = idx / CPRW8, c = (idx % CPRW8) * 8;
         const int m = m0 + p * RPP + row, n = n0 + c;
         if (m >= M || n >= N) continue;
         float v[8];
         ld_tile8(row, c, v);
-        epilogue8<E>(a, m, n, v);
+        epilogue8<E>(a, m, n, v, cbias + c, ax[i]);
+      }
+    } else {
+      static_assert(NCH8 % NT == 0, "whole passes");
+#pragma unroll 2
+      for (int idx = tid; idx < NCH8; idx += NT) {
+        const int row = idx / CPRW8, c = (idx % CPRW8) * 8;
+        const int m = m0 + p * RPP + row, n = n0 + c;
+        if (m >= M || n >= N) continue;
+        float v[8];
+        ld_tile8(row, c, v);
+        epilogue8<E>(a, m, n, v, cbias + c, nullptr);
       }
     }
     if (p + 1 < BM / RPP) {
@@ -582,13 +656,15 @@ __device__ __forceinline__ void gemm_f32_body(const GemmArgs& a) {
 }
 
 // ---------------------------------------------------------------- named kernels
+// Two-stage 4-wave tiles run two workgroups per CU (LDS <= 80 KB), so their
+// registers must fit two waves per SIMD; the bound says so to the compiler.
 #define RG_GEMM_KERNELS(NAME)                                                        \
   template <int BM, int BN, int WM, int WN, Epi E>                                   \
   __global__ __launch_bounds__(256) void NAME(GemmArgs a) {                          \
     gemm_bf16_body<BM, BN, WM, WN, E>(a);                                            \
   }                                                                                  \
   template <int BM, int BN, int WM, int WN, int NS, Epi E>                           \
-  __global__ __launch_bounds__(256) void NAME##_pipe(GemmArgs a) {                   \
+  __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void NAME##_pipe(GemmArgs a) {  \
     gemm_bf16_pipe_body<BM, BN, WM, WN, 64, NS, E, 4>(a);                            \
   }                                                                                  \
   template <int BM, int BN, int WM, int WN, int NS, Epi E>                           \
