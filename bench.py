@@ -28,8 +28,8 @@ PEAK_HBM_GBS = 8000.0       # MI355X HBM3E, published
 GEMM_PREFIX = "gemm_"
 CSRC = os.path.join(ROOT, "paper_2502_19864_amd", "csrc")
 # source files that define each family of named kernels
-KERNEL_SOURCES = {"gemm_": ("k_gemm.hip", "common.h", "kernels.h"),
-                  "attn_": ("k_attention.hip", "common.h", "kernels.h"),
+KERNEL_SOURCES = {"gemm_": ("k_gemm.hip", "attn_core.h", "common.h", "kernels.h"),
+                  "attn_": ("k_attention.hip", "attn_core.h", "common.h", "kernels.h"),
                   "adapter_": ("k_adapter.hip", "k_misc.hip", "common.h", "kernels.h")}
 
 

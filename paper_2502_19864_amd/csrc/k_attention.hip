@@ -15,24 +15,13 @@
 //
 // Log-sum-exp is kept in base 2 of the scaled scores: lse2 = log2 sum_j
 // 2^(s_j * scale * log2 e).
+#include "attn_core.h"
 #include "common.h"
 #include "kernels.h"
 
 namespace rg {
 
-constexpr float kLog2e = 1.4426950408889634f;
-
-// cos and sin of the rotation angle pos * theta^(-2i/dh) of pair i, from the
-// stage's table [max_seq][dh/2] (computed once in double precision)
-__device__ __forceinline__ void rope_cs(const float2* tab, int pos, int i, int dh, float* c, float* s) {
-  const float2 v = tab[(long)pos * (dh / 2) + i];
-  *c = v.x;
-  *s = v.y;
-}
-
 // ================================================================ bf16 / MFMA
-constexpr int KT = 128;      // keys (or queries) per LDS tile: a whole 128-token sequence in one
-
 // Loads two [KT x DH] tiles of rows r0.. (rows >= S are zero), e.g. K and V,
 // from column blocks col0 / col1 into LDS row-major (pitch DH + 8), rotating
 // pairs (i, i + DH/2) of the first when rot0.  Every global load of both tiles
@@ -115,55 +104,6 @@ __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool va
   for (int s = 0; s < DH / 16; ++s) f[s] = pack_frag(x[s]);
 }
 
-// A-operand fragment of (tile^T): rows = dims db*32 + lane%32 of a row-major
-// [row][dim] LDS tile, k = the 8 permuted rows matching register values
-// r = 8j..8j+7 of score block kb (rows kb*32 + 16j + 4*half + {0..3, 8..11}).
-template <int DH>
-__device__ __forceinline__ bf16x8 perm_frag(const bf16* tile, int db, int kb, int j, int lane) {
-  const int g = lane >> 4, dims = db * 32 + 16 * (g & 1), rows = kb * 32 + 16 * j + 4 * (g >> 1);
-  const uint2 lo = lds_tr4(tile, DH + 8, rows, dims, lane), hi = lds_tr4(tile, DH + 8, rows + 8, dims, lane);
-  return __builtin_bit_cast(bf16x8, make_uint4(lo.x, lo.y, hi.x, hi.y));
-}
-
-__device__ __forceinline__ bf16x8 pack8(const f32x16& v, int j) {
-  float t[8];
-#pragma unroll
-  for (int i = 0; i < 8; ++i) t[i] = v[8 * j + i];
-  return pack_frag(t);
-}
-
-// position of register value r within a 32-wide score block for this lane half
-__device__ __forceinline__ int perm_pos(int r, int half) { return 8 * (r >> 2) + 4 * half + (r & 3); }
-
-// Writes a 32-row x DH accumulator (transposed layout: lane = row, dims
-// 8*(r/4) + 4*half + r%4 of block db) scaled, optionally un-rotated.
-template <int DH>
-__device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, bool unrot, int pos,
-                                           const float2* rtab, int half, bf16* dst) {
-  if (unrot) {
-#pragma unroll
-    for (int db = 0; db < DH / 64; ++db)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int i = db * 32 + perm_pos(r, half);
-        float cs, sn;
-        rope_cs(rtab, pos, i, DH, &cs, &sn);
-        const float d1 = acc[db][r], d2 = acc[db + DH / 64][r];
-        acc[db][r] = d1 * cs + d2 * sn;
-        acc[db + DH / 64][r] = d2 * cs - d1 * sn;
-      }
-  }
-#pragma unroll
-  for (int db = 0; db < DH / 32; ++db)
-#pragma unroll
-    for (int g = 0; g < 4; ++g) {
-      float v[4];
-#pragma unroll
-      for (int q = 0; q < 4; ++q) v[q] = acc[db][4 * g + q] * scale;
-      St<bf16>::st4(dst, db * 32 + 8 * g + 4 * half, v);
-    }
-}
-
 template <int DH, bool CAUSAL, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
@@ -179,7 +119,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
 
   bf16x8 qf[DH / 16];
-  load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * DH, q, qv, a.rope,
+  load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * a.qkv_hs, q, qv, a.rope,
                      rtab, half, qf);
 
   f32x16 oacc[DH / 32];
@@ -193,7 +133,8 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
+                                a.qkv_vo + hd * a.qkv_hs, sV, b, S,
                                 kt * KT, rtab);
     __syncthreads();
     f32x16 sc[KT / 32];
@@ -277,7 +218,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const long qrow = (long)(b * S + (qv ? q : 0));
 
   bf16x8 qf[DH / 16], df[DH / 16];
-  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * DH, q, qv, a.rope, rtab, half, qf);
+  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * a.qkv_hs, q, qv, a.rope, rtab, half, qf);
   load_row_frags<DH>(static_cast<const bf16*>(a.dout) + qrow * a.ld_do + hd * DH, q, qv, false,
                      nullptr, half, df);
   float dsum = 0.f;
@@ -310,7 +251,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     // every query of the workgroup and every key of the tile in range, no causal mask
     const bool full = !CAUSAL && (qb + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
+                                a.qkv_vo + hd * a.qkv_hs, sV, b, S,
                                 kt * KT, rtab);
     __syncthreads();
     // one key block at a time (not unrolled): keeps the kernel within the
@@ -366,8 +308,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const long krow = (long)(b * S + (kv ? key : 0));
 
   bf16x8 kf[DH / 16], vf[DH / 16];
-  load_row_frags<DH>(qkv + krow * a.ld_qkv + d + hd * DH, key, kv, a.rope, rtab, half, kf);
-  load_row_frags<DH>(qkv + krow * a.ld_qkv + 2 * d + hd * DH, key, kv, false, nullptr, half, vf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + a.qkv_ko + hd * a.qkv_hs, key, kv, a.rope, rtab, half, kf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + a.qkv_vo + hd * a.qkv_hs, key, kv, false, nullptr, half, vf);
 
   f32x16 dk[DH / 32], dv[DH / 32];
 #pragma unroll
@@ -381,7 +323,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     // every key of the workgroup and every query of the tile in range, no causal mask
     const bool full = !CAUSAL && (kb0 + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
                                 rtab);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
@@ -455,8 +397,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const bf16* dO = static_cast<const bf16*>(a.dout);
 
   // Q, dO, K, V tiles (rows >= S zero); RoPE on Q and K
-  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * DH, a.rope, sQ, dO, a.ld_do, hd * DH, sdO, b, S, 0, rtab);
-  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, d + hd * DH, a.rope, sK, qkv, a.ld_qkv, 2 * d + hd * DH, sV, b, S, 0,
+  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, a.rope, sQ, dO, a.ld_do, hd * DH, sdO, b, S, 0, rtab);
+  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
+                                a.qkv_vo + hd * a.qkv_hs, sV, b, S, 0,
                               rtab);
 
   // this lane's query: its D = rowsum(dO * O) and LSE
@@ -743,6 +686,10 @@ static hipError_t check(int dtype, const AttnArgs& a, bool bwd) {
   if (a.B <= 0 || a.S <= 0 || a.H <= 0 || !a.qkv || !a.o || !a.lse) return hipErrorInvalidValue;
   if (bwd && (!a.dout || !a.dsum || !a.dqkv)) return hipErrorInvalidValue;
   if (a.rope && (!a.rope_tab || a.rope_rows < a.S)) return hipErrorInvalidValue;
+  const int d = a.H * a.dh;
+  const bool three_block = a.qkv_hs == a.dh && a.qkv_ko == d && a.qkv_vo == 2 * d;
+  const bool per_head = a.qkv_hs == 3 * a.dh && a.qkv_ko == a.dh && a.qkv_vo == 2 * a.dh;
+  if (!three_block && !(per_head && dtype == DT_BF16)) return hipErrorInvalidValue;
   if (dtype == DT_BF16) {
     if (a.dh != 64 && a.dh != 128) return hipErrorInvalidValue;
     if (a.ld_qkv % 8 || a.ld_o % 8 || !al16(a.qkv) || !al16(a.o)) return hipErrorInvalidValue;
@@ -753,7 +700,18 @@ static hipError_t check(int dtype, const AttnArgs& a, bool bwd) {
   return hipSuccess;
 }
 
-hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
+// the three-block Q | K | V order when no per-head layout is given
+static AttnArgs with_layout(AttnArgs a) {
+  if (a.qkv_hs == 0 && a.qkv_ko == 0 && a.qkv_vo == 0) {
+    a.qkv_hs = a.dh;
+    a.qkv_ko = a.H * a.dh;
+    a.qkv_vo = 2 * a.H * a.dh;
+  }
+  return a;
+}
+
+hipError_t launch_attn_fwd(int dtype, const AttnArgs& a0, hipStream_t s) {
+  const AttnArgs a = with_layout(a0);
   hipError_t e = check(dtype, a, false);
   if (e != hipSuccess) return e;
   if (dtype == DT_BF16) return a.dh == 64 ? fwd_dh<64>(a, s) : fwd_dh<128>(a, s);
@@ -761,7 +719,8 @@ hipError_t launch_attn_fwd(int dtype, const AttnArgs& a, hipStream_t s) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_bwd(int dtype, const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attn_bwd(int dtype, const AttnArgs& a0, hipStream_t s) {
+  const AttnArgs a = with_layout(a0);
   hipError_t e = check(dtype, a, true);
   if (e != hipSuccess) return e;
   if (dtype == DT_BF16) return a.dh == 64 ? bwd_dh<64>(a, s) : bwd_dh<128>(a, s);

@@ -14,6 +14,7 @@
 
 #include <utility>
 
+#include "attn_core.h"
 #include "common.h"
 #include "kernels.h"
 
@@ -370,7 +371,7 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
   // per pass through the stage buffers; the tile's bias columns (fp32) sit
   // at the end of those buffers, past the staging rows
   constexpr int CPF = BN + 4;
-  constexpr bool HAS_BIAS = E == Epi::Store || E == Epi::Gelu;
+  constexpr bool HAS_BIAS = E == Epi::Store || E == Epi::Gelu || E == Epi::Attn;
   constexpr int BIASB = HAS_BIAS ? BN * 4 : 0;
   constexpr int RPP = epi_rows(BM, CPF * 4, NS * STAGE - BIASB);
   static_assert(RPP >= 32 && BM % RPP == 0 && RPP * CPF * 4 + BIASB <= NS * STAGE,
@@ -534,6 +535,45 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
       *reinterpret_cast<float4*>(cbias + tid * 8) = make_float4(f[0], f[1], f[2], f[3]);
       *reinterpret_cast<float4*>(cbias + tid * 8 + 4) = make_float4(f[4], f[5], f[6], f[7]);
     }
+  if constexpr (E == Epi::Attn) {
+    // The tile is Q_h | K_h | V_h of one 128-token sequence: the sums (+ bias)
+    // go to three bf16 [128][64 + 8] LDS tiles (each lane holds four
+    // consecutive columns of one row), the projections to global memory when
+    // the caller keeps them, then each wave computes attention for 32 of the
+    // sequence's queries from those tiles.
+    static_assert(BM == KT && BN == 192 && WM == 2 && WN == 2 && NT == 256, "one head of one sequence per tile");
+    constexpr int DHA = 64, TPA = DHA + 8, TILE = BM * TPA;
+    static_assert(3 * TILE * 2 + BIASB <= NS * STAGE, "Q, K, V tiles and the bias fit the stage buffers");
+    bf16* sT = reinterpret_cast<bf16*>(smem);
+    barrier();  // the bias is in LDS
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          const int row = wm * TM + i * 32 + l32, col = wn * TN + j * 32 + 8 * g + 4 * half;
+          const float4 bb = a.bias ? *reinterpret_cast<const float4*>(cbias + col) : make_float4(0.f, 0.f, 0.f, 0.f);
+          const float v[4] = {acc[i][j][4 * g] + bb.x, acc[i][j][4 * g + 1] + bb.y, acc[i][j][4 * g + 2] + bb.z,
+                              acc[i][j][4 * g + 3] + bb.w};
+          St<bf16>::st4(sT + (col / DHA) * TILE + row * TPA, col % DHA, v);
+        }
+    wait_vm_lgkm<0>();
+    barrier();
+    if (a.out) {
+      constexpr int CPRA = BN / 8;
+#pragma unroll 4
+      for (int idx = tid; idx < BM * CPRA; idx += NT) {
+        const int row = idx / CPRA, q = idx % CPRA, part = q / (DHA / 8), c = (q % (DHA / 8)) * 8;
+        *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.out) + (long)(m0 + row) * a.ldo + n0 + part * DHA + c) =
+            *reinterpret_cast<const bf16x8*>(sT + part * TILE + row * TPA + c);
+      }
+    }
+    const int h = n0 / BN, H = N / BN, seq = m0 / BM;
+    bf16* orow = static_cast<bf16*>(a.out2) + (long)(m0 + wave * 32 + l32) * a.ldo2 + h * DHA;
+    attn_seq128_wave<DHA>(sT, sT + TILE, sT + 2 * TILE, wave * 32, lane, orow, a.lse + (long)(seq * H + h) * BM);
+    return;
+  }
   auto ld_tile8 = [&](int row, int col, float v[8]) {
     const float4 lo = *reinterpret_cast<const float4*>(cf + row * CPF + col);
     const float4 hi = *reinterpret_cast<const float4*>(cf + row * CPF + col + 4);
@@ -694,7 +734,8 @@ const char* role_name(Role r) {
 // epilogues each call site uses (only these are instantiated)
 static constexpr bool role_has(Role r, Epi e) {
   switch (r) {
-    case R_QKV_FWD: case R_O_FWD: case R_FFN_OUT_FWD: case R_O_DX: return e == Epi::Store;
+    case R_QKV_FWD: return e == Epi::Store || e == Epi::Attn;
+    case R_O_FWD: case R_FFN_OUT_FWD: case R_O_DX: return e == Epi::Store;
     case R_FFN_IN_FWD: return e == Epi::Gelu || e == Epi::SwiGlu;
     case R_QKV_DX: case R_FFN_IN_DX: return e == Epi::Resid || e == Epi::Store;
     case R_FFN_OUT_DX: return e == Epi::DGelu || e == Epi::DSwiGlu;
@@ -725,6 +766,10 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
     return hipErrorInvalidValue;
   } else {
     const dim3 block(256);
+    if constexpr (E == Epi::Attn) {  // bf16, 128x192 tiles only (checked by the caller)
+      RG_LAUNCH((gemm_qkv_fwd_pipe<128, 192, 2, 2, 2, Epi::Attn>), dim3((a.N / 192) * (a.M / 128)), block, 0, s, a);
+      return hipGetLastError();
+    } else {
     if (dtype == DT_F32) {
       if constexpr (E == Epi::SwiGlu) return hipErrorInvalidValue;
       else {
@@ -787,6 +832,7 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
 #undef RG_LAUNCH_CFG
 #undef RG_TILES
     return hipGetLastError();
+    }
   }
 }
 
@@ -798,6 +844,7 @@ static hipError_t launch_epi(Epi e, Cfg cfg, int dtype, const GemmArgs& a, hipSt
     case Epi::Resid: return launch_role<R, Epi::Resid>(cfg, dtype, a, s);
     case Epi::DGelu: return launch_role<R, Epi::DGelu>(cfg, dtype, a, s);
     case Epi::SwiGlu: return launch_role<R, Epi::SwiGlu>(cfg, dtype, a, s);
+    case Epi::Attn: return launch_role<R, Epi::Attn>(cfg, dtype, a, s);
     case Epi::DSwiGlu: return launch_role<R, Epi::DSwiGlu>(cfg, dtype, a, s);
   }
   return hipErrorInvalidValue;
@@ -807,6 +854,17 @@ static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) 
 static bool al8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
 hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStream_t s) {
+  if (epi == Epi::Attn) {
+    // bf16 QKV projection, one head (d_head 64) of one 128-token sequence per
+    // 128x192 tile; 16-B rows everywhere, 32-bit operand byte offsets
+    const bool ok = dtype == DT_BF16 && role == R_QKV_FWD && a.M > 0 && a.M % 128 == 0 && a.N % 192 == 0 &&
+                    a.K % 64 == 0 && a.A && a.B && a.out2 && a.lse && a.lda >= a.K && a.ldb >= a.K &&
+                    a.lda % 8 == 0 && a.ldb % 8 == 0 && al16(a.A) && al16(a.B) && a.ldo2 % 8 == 0 &&
+                    al16(a.out2) && (!a.bias || al16(a.bias)) && (!a.out || (a.ldo % 8 == 0 && al16(a.out))) &&
+                    ((double)(a.M - 1) * a.lda + a.K) * 2 < 4294967296.0 &&
+                    ((double)(a.N - 1) * a.ldb + a.K) * 2 < 4294967296.0;
+    return ok ? launch_epi<R_QKV_FWD>(epi, C_P128x192, dtype, a, s) : hipErrorInvalidValue;
+  }
   if (a.M < 0 || a.N <= 0 || a.K <= 0 || !a.A || !a.B || !a.out) return hipErrorInvalidValue;
   if (a.M == 0) return hipSuccess;
   if (a.N % 4 || a.ldo % 4 || a.lda < a.K || a.ldb < a.K) return hipErrorInvalidValue;

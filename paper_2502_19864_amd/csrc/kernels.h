@@ -41,6 +41,10 @@ enum class Epi {
             // out2[m, f] = gate, out2[m, half + f] = up (if non-null)
   DSwiGlu,  // acc = d(act)[m, f]; aux = [gate | up]; out[m, f] = d gate,
             // out[m, half + f] = d up
+  Attn,     // bf16 QKV projection with B rows in per-head order [Q_h K_h V_h]
+            // (d_head 64) and M = sequences of 128 tokens: pre = acc + bias;
+            // out = pre (if non-null); out2[:, 64h..64h+63] = softmax(Q_h K_h^T / 8) V_h
+            // per sequence; lse[(seq * H + h) * 128 + query] (base 2, scaled scores)
 };
 
 struct GemmArgs {
@@ -52,6 +56,7 @@ struct GemmArgs {
   void* out; int ldo;
   void* out2; int ldo2;
   int half;
+  float* lse;  // Attn only
 };
 
 // Names of the GEMM call sites (each gets its own kernel symbol).
@@ -72,7 +77,12 @@ struct AttnArgs {
   float theta;
   const float2* rope_tab;       // rope: (cos, sin) of pos * theta^(-2i/dh), [rope_rows][dh/2]
   int rope_rows;                // positions the table covers (>= S)
-  const void* qkv; int ld_qkv;  // [B*S, ld] with Q at column 0, K at d, V at 2d
+  const void* qkv; int ld_qkv;  // [B*S, ld]: Q, K, V of every head
+  // columns of head h in qkv: Q at h * qkv_hs, K at qkv_ko + h * qkv_hs, V at
+  // qkv_vo + h * qkv_hs.  All zero: three blocks of d columns (Q | K | V),
+  // i.e. (dh, d, 2d); (3 dh, dh, 2 dh) is the per-head order [Q_h K_h V_h]
+  // (bf16 only).  dqkv is always in the three-block order.
+  int qkv_hs, qkv_ko, qkv_vo;
   void* o; int ld_o;            // [B*S, d]
   float* lse;                   // [B, H, S]
   // backward

@@ -229,7 +229,8 @@ extern "C" int32_t ringada_local_cutoff(int32_t n_tm, int32_t depth, int32_t fir
 struct BlockBind {
   bool bound = false;
   ringada_block_weights w{};
-  void* wt_qkv = nullptr;  // [3d, d]
+  void* wt_qkv = nullptr;  // [3d, d]; rows in per-head order [Q_h K_h V_h] when the stage fuses attention
+  void* bqkv = nullptr;    // b_qkv in that per-head order (else unused)
   void* wt_o = nullptr;    // [d, d]
   void* wt_in = nullptr;   // post-LN [F, d]; pre-RMS packed [2F, d]
   void* wt_out = nullptr;  // [d, F]
@@ -250,6 +251,12 @@ struct ringada_stage {
   std::vector<void*> allocs;
   AdapterSlot* slots_dev = nullptr;
   float2* rope_tab = nullptr;  // rotary (cos, sin) [max_seq][d_head/2], built at the first bind
+  // bf16 post-LN stages with d_head 64 keep Q, K, V in per-head column order
+  // [Q_h K_h V_h] (projection weight rows and bias permuted at bind): a
+  // 128x192 tile of the QKV projection is then one head of one sequence, and
+  // 128-token sequences take the attention in that GEMM's epilogue
+  bool qkv_per_head = false;
+  void* qkv_tmp = nullptr;     // [3d, d] transposed projection before its rows are permuted
   std::vector<AdapterSlot> slots;
   // state machine
   bool pending = false;
@@ -275,6 +282,8 @@ extern "C" ringada_status ringada_stage_create(const ringada_stage_desc* desc, r
   RG_TRY(check_desc(desc));
   ringada_stage* st = new ringada_stage();
   st->D = *desc;
+  st->qkv_per_head = desc->dtype == RINGADA_BF16 && desc->arch == RINGADA_ARCH_POSTLN_GELU &&
+                     desc->d_model == 64 * desc->n_heads;
   st->blocks.resize(desc->n_blocks);
   st->slots.assign(2 * desc->n_blocks, AdapterSlot{});
   if (hipGetDevice(&st->device) != hipSuccess) st->device = 0;
@@ -317,6 +326,7 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
   BlockBind& b = st->blocks[block];
   if (!b.wt_qkv) {
     RG_TRY(dalloc(st, 3 * d * d * es, &b.wt_qkv));
+    if (st->qkv_per_head) RG_TRY(dalloc(st, 3 * d * es, &b.bqkv));
     RG_TRY(dalloc(st, d * d * es, &b.wt_o));
     RG_TRY(dalloc(st, (post ? 1 : 2) * F * d * es, &b.wt_in));
     RG_TRY(dalloc(st, d * F * es, &b.wt_out));
@@ -338,7 +348,24 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
   b.w = *w;
   b.ad[0] = attn ? *attn : ringada_adapter{};
   b.ad[1] = *ffn;
-  RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), b.wt_qkv, s));
+  if (st->qkv_per_head) {
+    // row (or bias element) p*d + h*dh + i of the three-block order goes to
+    // (3h + p)*dh + i
+    if (!st->qkv_tmp) RG_TRY(dalloc(st, 3 * d * d * es, &st->qkv_tmp));
+    RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), st->qkv_tmp, s));
+    const size_t dh = d / D.n_heads;
+    for (int h = 0; h < D.n_heads; ++h)
+      for (int p = 0; p < 3; ++p) {
+        const size_t src = p * d + h * dh, dst = (3 * h + p) * dh;
+        RG_HIP(hipMemcpyAsync(static_cast<char*>(b.wt_qkv) + dst * d * es,
+                              static_cast<const char*>(st->qkv_tmp) + src * d * es, dh * d * es,
+                              hipMemcpyDeviceToDevice, s));
+        RG_HIP(hipMemcpyAsync(static_cast<char*>(b.bqkv) + dst * es, static_cast<const char*>(w->b_qkv) + src * es,
+                              dh * es, hipMemcpyDeviceToDevice, s));
+      }
+  } else {
+    RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), b.wt_qkv, s));
+  }
   RG_HIP(launch_transpose(dt, dt, w->w_o, (int)d, (int)d, b.wt_o, s));
   if (post) RG_HIP(launch_transpose(dt, dt, w->w_in, (int)d, (int)F, b.wt_in, s));
   else RG_HIP(launch_pack_swiglu(dt, w->w_in, (int)d, (int)F, b.wt_in, s));
@@ -495,14 +522,27 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
     }));
     xin = n1;
   }
-  RG_TRY(gemm(c, R_QKV_FWD, Epi::Store, T, 3 * d, d, xin, d, b.wt_qkv, d, qkv, 3 * d, b.w.b_qkv));
-  AttnArgs aa{};
-  aa.B = L.B; aa.S = L.S; aa.H = c.H; aa.dh = c.dh;
-  aa.causal = c.llama; aa.rope = c.llama; aa.theta = st->D.rope_theta;
-  aa.rope_tab = st->rope_tab; aa.rope_rows = st->D.max_seq;
-  aa.qkv = qkv; aa.ld_qkv = 3 * d; aa.o = o; aa.ld_o = d; aa.lse = lse;
   const double attn_flops = 4.0 * L.B * c.H * (double)L.S * L.S * c.dh * (c.llama ? 0.5 : 1.0);
-  RG_TRY(run(st, c.s, "attn_fwd", attn_flops, es * 4.0 * T * d, [&] { return launch_attn_fwd(c.dt, aa, c.s); }));
+  if (st->qkv_per_head && L.S == 128) {
+    // projection + attention in one kernel; the projections leave it only
+    // when the backward needs them
+    GemmArgs g{xin, d, b.wt_qkv, d, T, 3 * d, d, b.bqkv, nullptr, 0, SN(sb.qkv), 3 * d, o, d, 0};
+    g.lse = lse;
+    const double bytes = es * ((double)T * d + 3.0 * d * d + (g.out ? 3.0 * T * d : 0.0) + (double)T * d) +
+                         4.0 * L.B * c.H * L.S;
+    RG_TRY(run(st, c.s, "gemm_qkv_attn_fwd", 2.0 * T * 3.0 * d * d + attn_flops, bytes,
+               [&] { return launch_gemm(c.dt, R_QKV_FWD, Epi::Attn, g, c.s); }));
+  } else {
+    RG_TRY(gemm(c, R_QKV_FWD, Epi::Store, T, 3 * d, d, xin, d, b.wt_qkv, d, qkv, 3 * d,
+                st->qkv_per_head ? b.bqkv : b.w.b_qkv));
+    AttnArgs aa{};
+    aa.B = L.B; aa.S = L.S; aa.H = c.H; aa.dh = c.dh;
+    aa.causal = c.llama; aa.rope = c.llama; aa.theta = st->D.rope_theta;
+    aa.rope_tab = st->rope_tab; aa.rope_rows = st->D.max_seq;
+    aa.qkv = qkv; aa.ld_qkv = 3 * d; aa.o = o; aa.ld_o = d; aa.lse = lse;
+    if (st->qkv_per_head) { aa.qkv_hs = 3 * c.dh; aa.qkv_ko = c.dh; aa.qkv_vo = 2 * c.dh; }
+    RG_TRY(run(st, c.s, "attn_fwd", attn_flops, es * 4.0 * T * d, [&] { return launch_attn_fwd(c.dt, aa, c.s); }));
+  }
   RG_TRY(gemm(c, R_O_FWD, Epi::Store, T, d, d, o, d, b.wt_o, d, attn, d, b.w.b_o));
 
   AdapterFwdArgs fa{};
@@ -681,6 +721,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   at.causal = c.llama; at.rope = c.llama; at.theta = st->D.rope_theta;
   at.rope_tab = st->rope_tab; at.rope_rows = st->D.max_seq;
   at.qkv = c.S(sb.qkv); at.ld_qkv = 3 * d; at.o = c.S(sb.o); at.ld_o = d;
+  if (st->qkv_per_head) { at.qkv_hs = 3 * c.dh; at.qkv_ko = c.dh; at.qkv_vo = 2 * c.dh; }
   at.lse = static_cast<float*>(c.S(sb.lse));
   at.dout = c.W(L.dout); at.ld_do = d; at.dsum = static_cast<float*>(c.W(L.dsum));
   at.dqkv = c.W(L.dqkv); at.ld_dqkv = 3 * d;

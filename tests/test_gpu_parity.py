@@ -40,6 +40,10 @@ SMALL = {
                                    "dy", 2006, placement="ffn"),
     "tiny_single": Workload("tiny_single", "bert", "f32", 3, 128, 2, 512, 16, 37, 3, 1, "dy", 2007,
                             tiny_adapter_init=True, placement="ffn"),
+    # seq 128 at d_head 64: the attention runs in the QKV projection's epilogue
+    # (one 128x192 tile per head and sequence), here on only 8 tiles; at the
+    # cut-off c = 1 block 0 keeps no projections, at c = -1 every block does
+    "small_bert_s128": Workload("small_bert_s128", "bert", "bf16", 3, 256, 4, 512, 64, 128, 2, 1, "dy", 2011),
 }
 
 
