@@ -157,8 +157,13 @@ def main():
     dx = st.empty(*inp["x"].shape) if c < 0 else None
     loss = torch.zeros(1, dtype=torch.float32, device=dev)
     if w.loss == "cls_ce":
-        wh, bh = st.f32(inp["w_h"]), st.f32(inp["b_h"])
-        gwh, gbh = torch.zeros_like(wh), torch.zeros_like(bh)
+        # the head's weight and bias in one buffer (and their gradients in
+        # another), so that one SGD launch updates both
+        nwh = inp["w_h"].size
+        hp = st.f32(np.concatenate([inp["w_h"].ravel(), inp["b_h"].ravel()]))
+        hg = torch.zeros_like(hp)
+        wh, bh = hp[:nwh].view(inp["w_h"].shape), hp[nwh:]
+        gwh, gbh = hg[:nwh].view(inp["w_h"].shape), hg[nwh:]
         labels = torch.from_numpy(inp["labels"]).to(dev)
     elif w.loss == "mse":
         target = st.upload(inp["target"])
@@ -172,8 +177,7 @@ def main():
         st.forward(x, y, c)
         if w.loss == "cls_ce":
             B.ringada_head_ce(s, st.desc.dtype, y, w.batch, w.seq, w.d_model, wh, bh, 2, labels, dy, gwh, gbh, loss)
-            B.ringada_sgd_f32(s, wh, gwh, wh.numel(), lr)
-            B.ringada_sgd_f32(s, bh, gbh, bh.numel(), lr)
+            B.ringada_sgd_f32(s, hp, hg, hp.numel(), lr)
         elif w.loss == "mse":
             B.ringada_loss_mse(s, st.desc.dtype, y, target, y.numel(), dy, loss)
         if c < w.n_blocks:
