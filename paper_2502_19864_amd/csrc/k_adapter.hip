@@ -355,11 +355,20 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 // workgroup.  Token-major tiles go to LDS as they are in memory (16-B chunks);
 // the MFMA operands, which need 8 consecutive tokens per lane, are read with
 // the LDS transpose read.
-constexpr int DW_TC = 256;
-__global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwArgs a) {
+// One launch covers up to DW_BATCH adapters: blockIdx.z = 2 * adapter + (0
+// up, 1 down).  512-token chunks: with a whole backward's adapters in one
+// launch there are workgroups enough, and each output element takes half the
+// atomic adds of 256-token chunks (1024 would hold every chunk's loads in
+// 256 registers).
+constexpr int DW_TC = 512, DW_BATCH = 16;
+struct AdapterDwBatch {
+  AdapterDwArgs a[DW_BATCH];
+};
+__global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
   __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [token][p]
   __shared__ __attribute__((aligned(16))) bf16 sY[64 * GP];  // [token][q]
-  const bool up = blockIdx.z == 0;
+  const AdapterDwArgs& a = batch.a[blockIdx.z >> 1];
+  const bool up = (blockIdx.z & 1) == 0;
   const int d = a.d, T = a.T;
   const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
   const bf16* Y = static_cast<const bf16*>(up ? a.dz : a.du);
@@ -832,15 +841,37 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
 hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s) {
   if (a.T < 0 || !a.u || !a.dz || !a.z || !a.du || !a.g_up || !a.g_down) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
-  if (dtype == DT_BF16) {
-    if (a.m != MB || a.d % 64) return hipErrorInvalidValue;
-    const dim3 grid(a.d / 64, (a.T + DW_TC - 1) / DW_TC, 2);
-    RG_LAUNCH(adapter_dw_bf16, grid, dim3(256), 0, s, a);
-    return hipGetLastError();
-  }
+  if (dtype == DT_BF16) return launch_adapter_dw_batch(dtype, &a, 1, s);
   const long n = 2L * a.m * a.d;
   RG_LAUNCH(adapter_dw_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
+}
+
+hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, hipStream_t s) {
+  if (n < 0 || (n > 0 && !a)) return hipErrorInvalidValue;
+  if (dtype != DT_BF16) {
+    for (int k = 0; k < n; ++k) {
+      const hipError_t e = launch_adapter_dw(dtype, a[k], s);
+      if (e != hipSuccess) return e;
+    }
+    return hipSuccess;
+  }
+  for (int k = 0; k < n; ++k) {
+    const AdapterDwArgs& x = a[k];
+    if (x.T < 0 || !x.u || !x.dz || !x.z || !x.du || !x.g_up || !x.g_down) return hipErrorInvalidValue;
+    if (x.T != a[0].T || x.d != a[0].d || x.m != a[0].m || x.m != MB || x.d % 64) return hipErrorInvalidValue;
+  }
+  if (n == 0 || a[0].T == 0) return hipSuccess;
+  for (int k0 = 0; k0 < n; k0 += DW_BATCH) {
+    const int nb = n - k0 < DW_BATCH ? n - k0 : DW_BATCH;
+    AdapterDwBatch b{};
+    for (int k = 0; k < nb; ++k) b.a[k] = a[k0 + k];
+    const dim3 grid(a[0].d / 64, (a[0].T + DW_TC - 1) / DW_TC, 2 * nb);
+    RG_LAUNCH(adapter_dw_bf16, grid, dim3(256), 0, s, b);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 }  // namespace rg

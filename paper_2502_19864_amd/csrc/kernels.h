@@ -150,6 +150,8 @@ struct AdapterDwArgs {
   float* g_down;   // [d, m]
 };
 hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s);
+// n adapters' weight gradients (same T, d, m) in as few launches as possible
+hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, hipStream_t s);
 
 // ---------------------------------------------------------------- row kernels
 // out = RMSNorm(x) * g, xhat/rstd stashes optional

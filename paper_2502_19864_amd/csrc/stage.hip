@@ -65,7 +65,11 @@ struct Layout {
   // forward scratch
   size_t act[2], h1, n1, n2, qkv, o, lse, attn, g, f2;
   // backward scratch (aliases the forward scratch: dead after the forward)
-  size_t dact[2], dz2, df2, da1, dh1, dz1, dattn, dout, dqkv, du, dsum, dn1;
+  size_t dact[2], df2, da1, dh1, dz1, dattn, dout, dqkv, dsum, dn1;
+  // per adapter in the backward, [2 l + a] (a = 0 attention, 1 FFN): the
+  // gradients at its output (dz) and at z W_down (du), kept until the one
+  // weight-gradient launch at the end of the backward
+  std::vector<size_t> gdz, gdu;
   size_t adp;  // both passes
 };
 
@@ -143,7 +147,6 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   cur = 0;  // backward scratch
   L.dact[0] = take(Td);
   L.dact[1] = take(Td);
-  L.dz2 = take(Td);
   L.df2 = take(Td);
   L.da1 = take(llama ? T2F : TF);
   L.dh1 = take(Td);
@@ -151,9 +154,17 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   L.dattn = take(Td);
   L.dout = take(Td);
   L.dqkv = take(T3d);
-  L.du = take(Tm);
   L.dsum = take(lse);
   L.dn1 = llama ? take(Td) : NONE;
+  L.gdz.assign(2 * D.n_blocks, NONE);
+  L.gdu.assign(2 * D.n_blocks, NONE);
+  for (int l = 0; l < D.n_blocks; ++l) {
+    if (block_kind(l, c, D.n_blocks) == K_NONE) continue;
+    for (int a = single ? 1 : 0; a < 2; ++a) {
+      L.gdz[2 * l + a] = take(Td);
+      L.gdu[2 * l + a] = take(Tm);
+    }
+  }
   // split-K partials of the wide (d > 1024) adapter kernels, used inside one
   // adapter call in either pass: after both lists
   const long part = adapter_part_elems(D.dtype, (int)T, (int)d, (int)m);
@@ -256,6 +267,9 @@ struct ringada_stage {
   // 128x192 tile of the QKV projection is then one head of one sequence, and
   // 128-token sequences take the attention in that GEMM's epilogue
   bool qkv_per_head = false;
+  // weight-gradient work of the adapters back-propagated so far in this
+  // backward, launched together when it ends
+  std::vector<AdapterDwArgs> dw_pending;
   void* qkv_tmp = nullptr;     // [3d, d] transposed projection before its rows are permuted
   std::vector<AdapterSlot> slots;
   // state machine
@@ -652,28 +666,30 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   const BlockStash& sb = L.blk[l];
   const int T = c.T, d = c.d, F = c.F, m = c.m;
   const double es = (double)c.es;
-  void* du = c.W(L.du);
-  const double ad_flops = 6.0 * T * d * m, dw_flops = 4.0 * T * d * m;
+  const double ad_flops = 6.0 * T * d * m;
   // under the single placement the block's lowest adapter is its FFN adapter
   const bool single = st->D.placement == RINGADA_PLACEMENT_FFN, stop_ffn = single && stop;
 
   // FFN adapter (+ LN2 for post-LN)
   AdapterBwdArgs ab{};
   ab.T = T; ab.d = d; ab.m = m; ab.gin = G; ab.u = c.S(sb.u2);
-  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = du; ab.dzin = stop_ffn ? nullptr : c.W(L.df2);
+  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = c.W(L.gdu[2 * l + 1]);
+  ab.dzin = stop_ffn ? nullptr : c.W(L.df2);
   ab.part = static_cast<float*>(c.W(L.adp));
-  const void* dz2;
+  // the gradient at the adapter output goes to this adapter's own buffer
+  // (pre-RMS: a copy of G, which a later block's dX overwrites)
+  ab.dz = c.W(L.gdz[2 * l + 1]);
+  const void* dz2 = ab.dz;
   if (c.llama) {
-    ab.norm = Norm::None; ab.dz = nullptr; dz2 = G;
+    ab.norm = Norm::None;
   } else {
     ab.norm = Norm::LN; ab.xhat = c.S(sb.xhat2); ab.rstd = static_cast<const float*>(c.S(sb.rstd2));
-    ab.gamma = b.w.norm2_g; ab.dz = c.W(L.dz2); dz2 = ab.dz;
+    ab.gamma = b.w.norm2_g;
   }
   RG_TRY(run(st, c.s, "adapter_bwd", stop_ffn ? 4.0 * T * d * m : ad_flops,
              es * ((c.llama ? 3.0 : 5.0) - (stop_ffn ? 1.0 : 0.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, ab, c.s); }));
-  AdapterDwArgs dw{T, d, m, c.S(sb.u2), dz2, c.S(sb.f2), du, b.ad[1].g_up, b.ad[1].g_down};
-  RG_TRY(run(st, c.s, "adapter_dw", dw_flops, es * 2.0 * T * d, [&] { return launch_adapter_dw(c.dt, dw, c.s); }));
+  st->dw_pending.push_back(AdapterDwArgs{T, d, m, c.S(sb.u2), dz2, c.S(sb.f2), ab.du, b.ad[1].g_up, b.ad[1].g_down});
   if (stop_ffn) return RINGADA_OK;
 
   // FFN (dX only through frozen weights)
@@ -691,13 +707,14 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   // placement) only the norm backward, whose output is then the gradient at
   // the attention sublayer's output
   AdapterBwdArgs aa{};
-  aa.T = T; aa.d = d; aa.m = m; aa.gin = c.W(L.dh1); aa.dz = c.W(L.dz1);
+  void* dz1 = single ? c.W(L.dz1) : c.W(L.gdz[2 * l]);
+  aa.T = T; aa.d = d; aa.m = m; aa.gin = c.W(L.dh1); aa.dz = dz1;
   aa.part = static_cast<float*>(c.W(L.adp));
   if (!single) {
-    aa.u = c.S(sb.u1); aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = du;
+    aa.u = c.S(sb.u1); aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = c.W(L.gdu[2 * l]);
     aa.dzin = stop ? nullptr : c.W(L.dattn);
   }
-  void* dattn = single ? c.W(L.dz1) : c.W(L.dattn);
+  void* dattn = single ? dz1 : c.W(L.dattn);
   if (c.llama) {
     aa.norm = Norm::RMS; aa.dres = G; aa.xhat = c.S(sb.xhat2);
     aa.rstd = static_cast<const float*>(c.S(sb.rstd2)); aa.gamma = b.w.norm2_g;
@@ -708,10 +725,8 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   RG_TRY(run(st, c.s, single ? "norm_bwd" : "adapter_bwd", single ? 0.0 : (stop ? 4.0 * T * d * m : ad_flops),
              es * ((c.llama ? 4.0 : 3.0) + (stop || single ? 0.0 : 1.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, aa, c.s); }));
-  if (!single) {
-    AdapterDwArgs dw1{T, d, m, c.S(sb.u1), c.W(L.dz1), c.S(sb.attn), du, b.ad[0].g_up, b.ad[0].g_down};
-    RG_TRY(run(st, c.s, "adapter_dw", dw_flops, es * 2.0 * T * d, [&] { return launch_adapter_dw(c.dt, dw1, c.s); }));
-  }
+  if (!single)
+    st->dw_pending.push_back(AdapterDwArgs{T, d, m, c.S(sb.u1), dz1, c.S(sb.attn), aa.du, b.ad[0].g_up, b.ad[0].g_down});
   if (stop) return RINGADA_OK;
 
   // attention (dX only)
@@ -730,12 +745,12 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   if (c.llama) {
     RG_TRY(gemm(c, R_QKV_DX, Epi::Store, T, d, 3 * d, c.W(L.dqkv), 3 * d, b.w.w_qkv, 3 * d, c.W(L.dn1), d));
     RG_TRY(run(st, c.s, "rms_bwd", 0, es * 4.0 * T * d, [&] {
-      return launch_rms_bwd(c.dt, T, d, c.W(L.dn1), c.W(L.dz1), c.S(sb.xhat1),
+      return launch_rms_bwd(c.dt, T, d, c.W(L.dn1), dz1, c.S(sb.xhat1),
                             static_cast<const float*>(c.S(sb.rstd1)), b.w.norm1_g, dX, c.s);
     }));
   } else {
     RG_TRY(gemm(c, R_QKV_DX, Epi::Resid, T, d, 3 * d, c.W(L.dqkv), 3 * d, b.w.w_qkv, 3 * d, dX, d, nullptr,
-                c.W(L.dz1), d));
+                dz1, d));
   }
   return RINGADA_OK;
 }
@@ -757,12 +772,20 @@ extern "C" ringada_status ringada_stage_backward(ringada_stage* st, void* stream
   RG_TRY(make_ctx(st, stream, cx));
   const void* G = dy;
   const int lo = c < 0 ? 0 : c;
+  st->dw_pending.clear();
   for (int l = D.n_blocks - 1; l >= lo; --l) {
     const bool stop = (l == c);
     void* dX = stop ? nullptr : (l == 0 ? dx_in : cx.W(st->L.dact[l % 2]));
     RG_TRY(block_backward(cx, l, G, dX, stop));
     G = dX;
   }
+  // the adapters' weight gradients (dW_up += gelu(U)^T dZ, dW_down += z^T dU)
+  // of the whole backward in one launch: off the dX chain, and enough
+  // workgroups to fill the GPU
+  const int ndw = (int)st->dw_pending.size();
+  RG_TRY(run(st, cx.s, "adapter_dw", 4.0 * ndw * cx.T * cx.d * cx.m, 2.0 * ndw * cx.es * cx.T * cx.d, [&] {
+    return launch_adapter_dw_batch(cx.dt, st->dw_pending.data(), ndw, cx.s);
+  }));
   st->pending = false;
   return RINGADA_OK;
 }
