@@ -22,57 +22,67 @@
 namespace rg {
 
 // ================================================================ bf16 / MFMA
-// Loads two [KT x DH] tiles of rows r0.. (rows >= S are zero), e.g. K and V,
-// from column blocks col0 / col1 into LDS row-major (pitch DH + 8), rotating
-// pairs (i, i + DH/2) of the first when rot0.  Every global load of both tiles
-// is issued before the first LDS store: the pair costs one memory round trip.
+// One [KT x DH] tile of rows r0.. (rows >= S are zero) from column col of a
+// row-major source into LDS row-major (pitch DH + 8), in two steps so that the
+// caller can issue the global loads of several tiles before the first LDS
+// store: issue() loads this thread's 16-B chunks into registers, store()
+// writes them, rotating pairs (i, i + DH/2) when rot.
+template <int DH, int NT>
+struct TileLoad {
+  static constexpr int HC = DH / 16, PAIRS = KT * HC, IT = PAIRS / NT;
+  static_assert(PAIRS % NT == 0, "whole passes of the workgroup");
+  bf16x8 raw[IT][2];
+  __device__ __forceinline__ void issue(const bf16* src, int ld, int col, int b, int S, int r0) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int p = threadIdx.x + it * NT;
+      const int r = p / HC, c = p % HC, row = r0 + r;
+      if (row < S) {
+        const bf16* a0 = src + (long)(b * S + row) * ld + col + c * 8;
+        raw[it][0] = ld_frag(a0);
+        raw[it][1] = ld_frag(a0 + DH / 2);
+      } else {
+        raw[it][0] = raw[it][1] = zero_frag();
+      }
+    }
+  }
+  __device__ __forceinline__ void store(bf16* dst, bool rot, int S, int r0, const float2* rtab) {
+#pragma unroll
+    for (int it = 0; it < IT; ++it) {
+      const int p = threadIdx.x + it * NT;
+      const int r = p / HC, c = p % HC, row = r0 + r;
+      if (rot && row < S) {
+        float x1[8], x2[8];
+        unpack_frag(raw[it][0], x1);
+        unpack_frag(raw[it][1], x2);
+#pragma unroll
+        for (int v = 0; v < 8; ++v) {
+          float cs, sn;
+          rope_cs(rtab, row, c * 8 + v, DH, &cs, &sn);
+          const float a = x1[v], bb = x2[v];
+          x1[v] = a * cs - bb * sn;
+          x2[v] = bb * cs + a * sn;
+        }
+        raw[it][0] = pack_frag(x1);
+        raw[it][1] = pack_frag(x2);
+      }
+      *reinterpret_cast<bf16x8*>(dst + r * (DH + 8) + c * 8) = raw[it][0];
+      *reinterpret_cast<bf16x8*>(dst + r * (DH + 8) + c * 8 + DH / 2) = raw[it][1];
+    }
+  }
+};
+
+// Two tiles (e.g. K and V) with one memory round trip: both tiles' global
+// loads are issued before the first LDS store; the first is rotated when rot0.
 template <int DH, int NT>
 __device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int col0, bool rot0, bf16* dst0,
                                                const bf16* src1, int ld1, int col1, bf16* dst1, int b, int S,
                                                int r0, const float2* rtab) {
-  constexpr int HC = DH / 16;
-  constexpr int PAIRS = KT * HC, IT = PAIRS / NT;
-  static_assert(PAIRS % NT == 0, "whole passes of the workgroup");
-  bf16x8 raw[2][IT][2];
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int p = threadIdx.x + it * NT;
-    const int r = p / HC, c = p % HC, row = r0 + r;
-    if (row < S) {
-      const bf16* a0 = src0 + (long)(b * S + row) * ld0 + col0 + c * 8;
-      const bf16* a1 = src1 + (long)(b * S + row) * ld1 + col1 + c * 8;
-      raw[0][it][0] = ld_frag(a0);
-      raw[0][it][1] = ld_frag(a0 + DH / 2);
-      raw[1][it][0] = ld_frag(a1);
-      raw[1][it][1] = ld_frag(a1 + DH / 2);
-    } else {
-      raw[0][it][0] = raw[0][it][1] = raw[1][it][0] = raw[1][it][1] = zero_frag();
-    }
-  }
-#pragma unroll
-  for (int it = 0; it < IT; ++it) {
-    const int p = threadIdx.x + it * NT;
-    const int r = p / HC, c = p % HC, row = r0 + r;
-    if (rot0 && row < S) {
-      float x1[8], x2[8];
-      unpack_frag(raw[0][it][0], x1);
-      unpack_frag(raw[0][it][1], x2);
-#pragma unroll
-      for (int v = 0; v < 8; ++v) {
-        float cs, sn;
-        rope_cs(rtab, row, c * 8 + v, DH, &cs, &sn);
-        const float a = x1[v], bb = x2[v];
-        x1[v] = a * cs - bb * sn;
-        x2[v] = bb * cs + a * sn;
-      }
-      raw[0][it][0] = pack_frag(x1);
-      raw[0][it][1] = pack_frag(x2);
-    }
-    *reinterpret_cast<bf16x8*>(dst0 + r * (DH + 8) + c * 8) = raw[0][it][0];
-    *reinterpret_cast<bf16x8*>(dst0 + r * (DH + 8) + c * 8 + DH / 2) = raw[0][it][1];
-    *reinterpret_cast<bf16x8*>(dst1 + r * (DH + 8) + c * 8) = raw[1][it][0];
-    *reinterpret_cast<bf16x8*>(dst1 + r * (DH + 8) + c * 8 + DH / 2) = raw[1][it][1];
-  }
+  TileLoad<DH, NT> t0, t1;
+  t0.issue(src0, ld0, col0, b, S, r0);
+  t1.issue(src1, ld1, col1, b, S, r0);
+  t0.store(dst0, rot0, S, r0, rtab);
+  t1.store(dst1, false, S, r0, rtab);
 }
 
 // Fragments (B operand, k = head dim) of one row held by this lane: dims
@@ -396,37 +406,40 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
   const bf16* dO = static_cast<const bf16*>(a.dout);
 
-  // Q, dO, K, V tiles (rows >= S zero); RoPE on Q and K
-  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, a.rope, sQ, dO, a.ld_do, hd * DH, sdO, b, S, 0, rtab);
-  load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
-                                a.qkv_vo + hd * a.qkv_hs, sV, b, S, 0,
-                              rtab);
-
-  // this lane's query: its D = rowsum(dO * O) and LSE
+  // Q, dO, K, V tiles (rows >= S zero; RoPE on Q and K), this lane's O row
+  // and its LSE, every global load issued before the first LDS store.  The
+  // prologue is bound by memory bandwidth (all workgroups load at once), so
+  // dO is read once: the row sum D = rowsum(dO * O) takes it from the tile.
   const int q = wave * 32 + l32;
   const bool qv = q < S;
   const long qrow = (long)(b * S + (qv ? q : 0));
-  float dsum = 0.f;
+  TileLoad<DH, 64 * NW> tq, tdo, tk, tv;
+  tq.issue(qkv, a.ld_qkv, hd * a.qkv_hs, b, S, 0);
+  tdo.issue(dO, a.ld_do, hd * DH, b, S, 0);
+  tk.issue(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, b, S, 0);
+  tv.issue(qkv, a.ld_qkv, a.qkv_vo + hd * a.qkv_hs, b, S, 0);
+  bf16x8 orw[DH / 16];
   {
     const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
-    const bf16* drow = dO + qrow * a.ld_do + hd * DH;
 #pragma unroll
-    for (int s = 0; s < DH / 16; ++s) {
-      float ov[8], dv[8];
-      if (qv) {
-        unpack_frag(ld_frag(orow + 16 * s + 8 * half), ov);
-        unpack_frag(ld_frag(drow + 16 * s + 8 * half), dv);
-      } else {
-#pragma unroll
-        for (int v = 0; v < 8; ++v) ov[v] = dv[v] = 0.f;
-      }
-#pragma unroll
-      for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
-    }
-    dsum += __shfl_xor(dsum, 32, 64);
+    for (int s = 0; s < DH / 16; ++s) orw[s] = qv ? ld_frag(orow + 16 * s + 8 * half) : zero_frag();
   }
   const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
+  tq.store(sQ, a.rope, S, 0, rtab);
+  tdo.store(sdO, false, S, 0, rtab);
+  tk.store(sK, a.rope, S, 0, rtab);
+  tv.store(sV, false, S, 0, rtab);
   __syncthreads();
+  float dsum = 0.f;
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) {
+    float ov[8], dv[8];
+    unpack_frag(orw[s], ov);
+    unpack_frag(ld_frag(sdO + q * (DH + 8) + 16 * s + 8 * half), dv);  // rows >= S are zero
+#pragma unroll
+    for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
+  }
+  dsum += __shfl_xor(dsum, 32, 64);
 
   // ---- scores, P, dS and dQ (lane = query)
   const bool full = !CAUSAL && S == KT;
