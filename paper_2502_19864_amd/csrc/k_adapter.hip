@@ -190,37 +190,33 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 }
 
 // ================================================================ bf16 backward, d <= 1024
-// One workgroup of 16 waves per 16 tokens: the norm backward (row sums over
-// the waves through LDS), dV = dZ W_up^T (k split over 4 waves), dU = dV *
-// gelu'(U), and dzin = dZ + dU W_down^T, with every weight fragment loaded
-// while the previous phase runs.
+// One workgroup of 16 waves per 16 tokens.
+//  1. The norm backward with one wave per token: every global row access is a
+//     contiguous 512-B run per instruction and the row sums are wave
+//     reductions; dz stays in fp32 registers and goes to LDS (bf16) for
+//     2. dV = dZ W_up^T (k split over 4 waves, MFMA, lane = token), dU =
+//     dV * gelu'(U);
+//  3. dU W_down^T (MFMA), staged in LDS as fp32, then dzin = dz + that, again
+//     one wave per token.
+// Every weight fragment is loaded while the previous phase runs.
 template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int KS = NW / 4;
-  constexpr int D = 16 * NW * FB, DP = D + 8, SLICE = D / KS;
+  constexpr int D = 16 * NW * FB, DP = D + 8, VP = D + 4, SLICE = D / KS;
+  static_assert(NW == TOK, "one wave per token in the row phases");
+  static_assert(D == 256 * FB, "four consecutive features per lane, FB runs of 256");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* sdZ = reinterpret_cast<bf16*>(smem);                       // [TOK][DP]
   bf16* sdU = sdZ + TOK * DP;                                      // [TOK][GP]
   float* sPart = reinterpret_cast<float*>(sdU + TOK * GP);         // [KS][TOK][MB]
-  float* sRed = sPart + KS * TOK * MB;                             // [NW][TOK]
+  float* sV = sPart + KS * TOK * MB;                               // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T;
-  const int token = blockIdx.x * TOK + l16;
+  const int token = blockIdx.x * TOK + l16;  // this lane's token in the MFMA phases
   const bool tv = token < T;
-  const long trow = (long)(tv ? token : 0) * D;
-  const int f0 = wave * 16 * FB;
-
-  auto row_sum = [&](float s) {
-    s += __shfl_xor(s, 16, 64);
-    s += __shfl_xor(s, 32, 64);
-    if (grp == 0) sRed[wave * TOK + l16] = s;
-    __syncthreads();
-    float t = 0.f;
-#pragma unroll
-    for (int w = 0; w < NW; ++w) t += sRed[w * TOK + l16];
-    __syncthreads();
-    return t;
-  };
+  const int tw = blockIdx.x * TOK + wave;    // this wave's token in the row phases
+  const bool twv = tw < T;
+  const long wrow = (long)(twv ? tw : 0) * D;
 
   // fragments of W_up for the first contraction: in flight during the norm backward
   const int ug = wave % 4, ks = wave / 4;
@@ -228,69 +224,65 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   static_assert(FB <= 4, "d <= 1024: every weight fragment fits the registers (wider widths split the work)");
   const bool has_ad = a.wup != nullptr;  // else: the norm backward only
   bf16x8 wup_f[NSTEP];
-  {
-    if (has_ad) {
+  if (has_ad) {
 #pragma unroll
-      for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
-    }
+    for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
   }
-
   // pre-activation of this lane's four units (read in the dV phase), loaded now
   const int ug0 = (wave % 4) * 16 + 4 * grp;
   uint2 uraw = make_uint2(0, 0);
   if (has_ad && tv && wave < 4) uraw = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.u) + (long)token * MB + ug0);
 
-  // ---- gradient at the adapter output (all loads issued up front)
+  // ---- gradient at the adapter output, one wave per token (features 4 lane + 256 j)
   float dz[FB][4];
   {
-    float gg[FB][4], xh[FB][4], dr[FB][4];
+    float gg[FB][4], xh[FB][4], dr[FB][4], gm[FB][4];
 #pragma unroll
-    for (int b = 0; b < FB; ++b) {
-      const long o = trow + f0 + b * 16 + 4 * grp;
+    for (int j = 0; j < FB; ++j) {
+      const int f = 4 * lane + 256 * j;
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gg[b][q] = xh[b][q] = dr[b][q] = 0.f;
-      if (tv) {
-        St<bf16>::ld4(static_cast<const bf16*>(a.gin), o, gg[b]);
-        if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), o, xh[b]);
-        if (a.norm == Norm::RMS) St<bf16>::ld4(static_cast<const bf16*>(a.dres), o, dr[b]);
+      for (int q = 0; q < 4; ++q) gg[j][q] = xh[j][q] = dr[j][q] = gm[j][q] = 0.f;
+      if (twv) {
+        St<bf16>::ld4(static_cast<const bf16*>(a.gin), wrow + f, gg[j]);
+        if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), wrow + f, xh[j]);
+        if (a.norm == Norm::RMS) St<bf16>::ld4(static_cast<const bf16*>(a.dres), wrow + f, dr[j]);
       }
+      if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm[j]);
     }
-    const float rs = (tv && a.norm != Norm::None) ? a.rstd[token] : 0.f;
+    const float rs = (twv && a.norm != Norm::None) ? a.rstd[tw] : 0.f;
     if (a.norm == Norm::None) {
 #pragma unroll
-      for (int b = 0; b < FB; ++b)
+      for (int j = 0; j < FB; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) dz[b][q] = gg[b][q];
+        for (int q = 0; q < 4; ++q) dz[j][q] = gg[j][q];
     } else {
       float s1 = 0.f, s2 = 0.f;
 #pragma unroll
-      for (int b = 0; b < FB; ++b) {
-        float gm[4];
-        St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f0 + b * 16 + 4 * grp, gm);
+      for (int j = 0; j < FB; ++j)
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-          gg[b][q] *= gm[q];
-          s1 += gg[b][q];
-          s2 += gg[b][q] * xh[b][q];
+          gg[j][q] *= gm[j][q];
+          s1 += gg[j][q];
+          s2 += gg[j][q] * xh[j][q];
         }
-      }
       constexpr float inv_d = 1.f / (float)D;
-      const float m1 = (a.norm == Norm::LN) ? row_sum(s1) * inv_d : 0.f;
-      const float m2 = row_sum(s2) * inv_d;
+      const float m1 = (a.norm == Norm::LN) ? wave_sum(s1) * inv_d : 0.f;
+      const float m2 = wave_sum(s2) * inv_d;
 #pragma unroll
-      for (int b = 0; b < FB; ++b)
+      for (int j = 0; j < FB; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) dz[b][q] = dr[b][q] + rs * (gg[b][q] - m1 - xh[b][q] * m2);
+        for (int q = 0; q < 4; ++q) dz[j][q] = dr[j][q] + rs * (gg[j][q] - m1 - xh[j][q] * m2);
     }
   }
 #pragma unroll
-  for (int b = 0; b < FB; ++b) {
-    const int f = f0 + b * 16 + 4 * grp;
-    if (tv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), trow + f, dz[b]);
-    St<bf16>::st4(sdZ, (long)l16 * DP + f, dz[b]);
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    if (twv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), wrow + f, dz[j]);
+    St<bf16>::st4(sdZ, (long)wave * DP + f, dz[j]);
   }
   if (!has_ad) return;
   // W_down fragments of the last contraction, in flight during the dV one
+  const int f0 = wave * 16 * FB;
   bf16x8 w0[FB], w1[FB];
   if (a.dzin) {
 #pragma unroll
@@ -317,10 +309,10 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
       if (ks == 0) {
 #pragma unroll
         for (int r = 0; r < 4; ++r) {
-          float s = 0.f;
+          float sum = 0.f;
 #pragma unroll
-          for (int k2 = 0; k2 < KS; ++k2) s += sPart[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
-          dv[r] = s;
+          for (int k2 = 0; k2 < KS; ++k2) sum += sPart[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
+          dv[r] = sum;
         }
       }
     }
@@ -335,17 +327,25 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   if (!a.dzin) return;
   __syncthreads();
 
-  // ---- dzin^T[f][token] = dZ + W_down[f][:] . dU[token][:]
-  const bf16x8 u0 = ld_frag(sdU + l16 * GP + 8 * grp), u1 = ld_frag(sdU + l16 * GP + 32 + 8 * grp);
+  // ---- (dU W_down^T)^T[f][token] -> sV (fp32), then dzin = dz + sV, one wave per token
+  {
+    const bf16x8 u0 = ld_frag(sdU + l16 * GP + 8 * grp), u1 = ld_frag(sdU + l16 * GP + 32 + 8 * grp);
 #pragma unroll
-  for (int b = 0; b < FB; ++b) {
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    acc = mfma16(w0[b], u0, acc);
-    acc = mfma16(w1[b], u1, acc);
-    float o[4];
+    for (int b = 0; b < FB; ++b) {
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      acc = mfma16(w0[b], u0, acc);
+      acc = mfma16(w1[b], u1, acc);
+      *reinterpret_cast<float4*>(sV + l16 * VP + f0 + b * 16 + 4 * grp) = make_float4(acc[0], acc[1], acc[2], acc[3]);
+    }
+  }
+  __syncthreads();
+  if (!twv) return;
 #pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = dz[b][q] + acc[q];
-    if (tv) St<bf16>::st4(static_cast<bf16*>(a.dzin), trow + f0 + b * 16 + 4 * grp, o);
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    const float4 v = *reinterpret_cast<const float4*>(sV + wave * VP + f);
+    const float o[4] = {dz[j][0] + v.x, dz[j][1] + v.y, dz[j][2] + v.z, dz[j][3] + v.w};
+    St<bf16>::st4(static_cast<bf16*>(a.dzin), wrow + f, o);
   }
 }
 
@@ -720,7 +720,7 @@ template <int NW, int FB>
 static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
   constexpr int D = 16 * NW * FB;
   const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
-                    (size_t)NW * TOK * 4;
+                    (size_t)TOK * (D + 4) * 4;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_bwd_bf16<NW, FB>),
