@@ -415,6 +415,7 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
   }
   static_assert(HEAD_SPW * 64 == 256, "one wave per sample of the workgroup");
   __shared__ float sdl[HEAD_SPW][CN];
+  __shared__ float sloss[HEAD_SPW];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int j0 = blockIdx.x * HEAD_SPW, j = j0 + wave;
   if (j < B) {
@@ -459,19 +460,29 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
         if (c == lab) ll = lg[c];
       }
     if (lane == 0) {
-      if (loss) unsafeAtomicAdd(loss, -(ll - mx - __logf(se)) / (float)B);
+      sloss[wave] = -(ll - mx - __logf(se)) / (float)B;
 #pragma unroll
       for (int c = 0; c < CN; ++c)
-        if (c < C) {
-          const float g = (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B;
-          sdl[wave][c] = g;
-          unsafeAtomicAdd(gbh + c, g);
-        }
+        sdl[wave][c] = c < C ? (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B : 0.f;
     }
   } else if (lane < CN) {
     sdl[wave][lane] = 0.f;
+    if (lane == 0) sloss[wave] = 0.f;
   }
   __syncthreads();
+  // the workgroup's samples summed first: one atomic add per address per
+  // workgroup (adds to one address are serialised in memory)
+  if (threadIdx.x <= CN) {
+    const int c = threadIdx.x;
+    float t = 0.f;
+#pragma unroll
+    for (int w = 0; w < HEAD_SPW; ++w) t += c == CN ? sloss[w] : sdl[w][c];
+    if (c == CN) {
+      if (loss) unsafeAtomicAdd(loss, t);
+    } else if (c < C) {
+      unsafeAtomicAdd(gbh + c, t);
+    }
+  }
   const int ns = min(HEAD_SPW, B - j0);
   for (int i = threadIdx.x; i < d; i += 256) {
     float w[CN], acc[CN], yi[HEAD_SPW];
