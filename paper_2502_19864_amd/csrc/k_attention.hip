@@ -85,6 +85,9 @@ __device__ __forceinline__ void load_tile_pair(const bf16* src0, int ld0, int co
   t1.store(dst1, false, S, r0, rtab);
 }
 
+// Q and K need the rotation as they are loaded (it is not already in qkv)
+__device__ __forceinline__ bool rot_load(const AttnArgs& a) { return a.rope && !a.rope_in_qkv; }
+
 // Fragments (B operand, k = head dim) of one row held by this lane: dims
 // 16s + 8*(lane/32) + v, rotated when rot.
 template <int DH>
@@ -129,7 +132,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const bf16* qkv = static_cast<const bf16*>(a.qkv);
 
   bf16x8 qf[DH / 16];
-  load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * a.qkv_hs, q, qv, a.rope,
+  load_row_frags<DH>(qkv + (long)(b * S + (qv ? q : 0)) * a.ld_qkv + hd * a.qkv_hs, q, qv, rot_load(a),
                      rtab, half, qf);
 
   f32x16 oacc[DH / 32];
@@ -143,7 +146,7 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, rot_load(a), sK, qkv, a.ld_qkv,
                                 a.qkv_vo + hd * a.qkv_hs, sV, b, S,
                                 kt * KT, rtab);
     __syncthreads();
@@ -228,7 +231,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const long qrow = (long)(b * S + (qv ? q : 0));
 
   bf16x8 qf[DH / 16], df[DH / 16];
-  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * a.qkv_hs, q, qv, a.rope, rtab, half, qf);
+  load_row_frags<DH>(qkv + qrow * a.ld_qkv + hd * a.qkv_hs, q, qv, rot_load(a), rtab, half, qf);
   load_row_frags<DH>(static_cast<const bf16*>(a.dout) + qrow * a.ld_do + hd * DH, q, qv, false,
                      nullptr, half, df);
   float dsum = 0.f;
@@ -261,7 +264,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     // every query of the workgroup and every key of the tile in range, no causal mask
     const bool full = !CAUSAL && (qb + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, a.rope, sK, qkv, a.ld_qkv,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, rot_load(a), sK, qkv, a.ld_qkv,
                                 a.qkv_vo + hd * a.qkv_hs, sV, b, S,
                                 kt * KT, rtab);
     __syncthreads();
@@ -318,7 +321,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const long krow = (long)(b * S + (kv ? key : 0));
 
   bf16x8 kf[DH / 16], vf[DH / 16];
-  load_row_frags<DH>(qkv + krow * a.ld_qkv + a.qkv_ko + hd * a.qkv_hs, key, kv, a.rope, rtab, half, kf);
+  load_row_frags<DH>(qkv + krow * a.ld_qkv + a.qkv_ko + hd * a.qkv_hs, key, kv, rot_load(a), rtab, half, kf);
   load_row_frags<DH>(qkv + krow * a.ld_qkv + a.qkv_vo + hd * a.qkv_hs, key, kv, false, nullptr, half, vf);
 
   f32x16 dk[DH / 32], dv[DH / 32];
@@ -333,7 +336,7 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     // every key of the workgroup and every query of the tile in range, no causal mask
     const bool full = !CAUSAL && (kb0 + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, a.rope, sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
+    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, rot_load(a), sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
                                 rtab);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
@@ -425,9 +428,9 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     for (int s = 0; s < DH / 16; ++s) orw[s] = qv ? ld_frag(orow + 16 * s + 8 * half) : zero_frag();
   }
   const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
-  tq.store(sQ, a.rope, S, 0, rtab);
+  tq.store(sQ, rot_load(a), S, 0, rtab);
   tdo.store(sdO, false, S, 0, rtab);
-  tk.store(sK, a.rope, S, 0, rtab);
+  tk.store(sK, rot_load(a), S, 0, rtab);
   tv.store(sV, false, S, 0, rtab);
   __syncthreads();
   float dsum = 0.f;
@@ -699,6 +702,7 @@ static hipError_t check(int dtype, const AttnArgs& a, bool bwd) {
   if (a.B <= 0 || a.S <= 0 || a.H <= 0 || !a.qkv || !a.o || !a.lse) return hipErrorInvalidValue;
   if (bwd && (!a.dout || !a.dsum || !a.dqkv)) return hipErrorInvalidValue;
   if (a.rope && (!a.rope_tab || a.rope_rows < a.S)) return hipErrorInvalidValue;
+  if (a.rope_in_qkv && (!a.rope || dtype != DT_BF16)) return hipErrorInvalidValue;
   const int d = a.H * a.dh;
   const bool three_block = a.qkv_hs == a.dh && a.qkv_ko == d && a.qkv_vo == 2 * d;
   const bool per_head = a.qkv_hs == 3 * a.dh && a.qkv_ko == a.dh && a.qkv_vo == 2 * a.dh;

@@ -626,6 +626,36 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
         ld_tile8(row, c + 32, uv);
         epilogue_swiglu8(a, m, (n0 + c) / 64 * 32 + (c % 64), gv, uv);
       }
+    } else if constexpr (E == Epi::Rope) {
+      // chunk pairs: 8 columns at head-local offset i < dh/2 and the 8 at
+      // i + dh/2; the tile spans whole heads (BN = 128, n0 a multiple of 128)
+      static_assert(BN == 128, "rotary epilogue on 128-wide tiles only");
+      constexpr int NPAIR = RPP * CPRW8 / 2;
+      static_assert(NPAIR % NT == 0, "whole passes");
+      const int dh = a.rope_dh, hc = dh / 16;  // pairs of chunks per head
+#pragma unroll 2
+      for (int idx = tid; idx < NPAIR; idx += NT) {
+        const int row = idx / (CPRW8 / 2), pr = idx % (CPRW8 / 2);
+        const int c1 = (pr / hc) * dh + (pr % hc) * 8, c2 = c1 + dh / 2;
+        const int m = m0 + p * RPP + row, n1 = n0 + c1, n2 = n0 + c2;
+        if (m >= M || n2 >= N) continue;
+        float v1[8], v2[8];
+        ld_tile8(row, c1, v1);
+        ld_tile8(row, c2, v2);
+        if (n1 < a.rope_cols) {
+          const float2* cs = a.rope_tab + (long)(m % a.rope_S) * (dh / 2) + (n1 % dh);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const float2 t = cs[e];
+            const float x1 = v1[e], x2 = v2[e];
+            v1[e] = x1 * t.x - x2 * t.y;
+            v2[e] = x2 * t.x + x1 * t.y;
+          }
+        }
+        bf16* out = static_cast<bf16*>(a.out);
+        st8(out + (long)m * a.ldo + n1, v1);
+        st8(out + (long)m * a.ldo + n2, v2);
+      }
     } else if constexpr (HAS_AUX) {
       static_assert(NCH8 % NT == 0, "whole passes");
 #pragma unroll
@@ -734,7 +764,7 @@ const char* role_name(Role r) {
 // epilogues each call site uses (only these are instantiated)
 static constexpr bool role_has(Role r, Epi e) {
   switch (r) {
-    case R_QKV_FWD: return e == Epi::Store || e == Epi::Attn;
+    case R_QKV_FWD: return e == Epi::Store || e == Epi::Attn || e == Epi::Rope;
     case R_O_FWD: case R_FFN_OUT_FWD: case R_O_DX: return e == Epi::Store;
     case R_FFN_IN_FWD: return e == Epi::Gelu || e == Epi::SwiGlu;
     case R_QKV_DX: case R_FFN_IN_DX: return e == Epi::Resid || e == Epi::Store;
@@ -771,7 +801,7 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       return hipGetLastError();
     } else {
     if (dtype == DT_F32) {
-      if constexpr (E == Epi::SwiGlu) return hipErrorInvalidValue;
+      if constexpr (E == Epi::SwiGlu || E == Epi::Rope) return hipErrorInvalidValue;
       else {
         dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
         switch (R) {
@@ -789,11 +819,11 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
 #define RG_LAUNCH_CFG(NAME)                                                                                  \
   switch (cfg) {                                                                                         \
     case C_P128x192:                                                                                     \
-      if constexpr (E != Epi::SwiGlu)                                                                    \
+      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
         RG_LAUNCH((NAME##_pipe<128, 192, 2, 2, 2, E>), RG_TILES(128, 192), block, 0, s, a);     \
       break;                                                                                             \
     case C_P128x96:                                                                                      \
-      if constexpr (E != Epi::SwiGlu)                                                                    \
+      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
         RG_LAUNCH((NAME##_pipe<128, 96, 4, 1, 3, E>), RG_TILES(128, 96), block, 0, s, a);       \
       break;                                                                                             \
     case C_P128x128_2:                                                                                   \
@@ -803,19 +833,21 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
       break;                                                                                             \
     case C_P256x192_8W:                                                                                  \
-      if constexpr (E != Epi::SwiGlu)                                                                    \
+      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
         RG_LAUNCH((NAME##_pipe8<256, 192, 4, 2, 2, E>), RG_TILES(256, 192), dim3(512), 0, s, a);          \
       break;                                                                                             \
     case C_P256x128_8W:                                                                                  \
       RG_LAUNCH((NAME##_pipe8<256, 128, 4, 2, 3, E>), RG_TILES(256, 128), dim3(512), 0, s, a);            \
       break;                                                                                             \
     case C_REG_128x128:                                                                                  \
-      RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
-                         s, a);                                                                          \
+      if constexpr (E != Epi::Rope)                                                                      \
+        RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
+                           s, a);                                                                        \
       break;                                                                                             \
     case C_REG_64x128:                                                                                   \
-      RG_LAUNCH((NAME<64, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 63) / 64), block, 0,   \
-                         s, a);                                                                          \
+      if constexpr (E != Epi::Rope)                                                                      \
+        RG_LAUNCH((NAME<64, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 63) / 64), block, 0,   \
+                           s, a);                                                                        \
       break;                                                                                             \
   }
     switch (R) {
@@ -845,6 +877,7 @@ static hipError_t launch_epi(Epi e, Cfg cfg, int dtype, const GemmArgs& a, hipSt
     case Epi::DGelu: return launch_role<R, Epi::DGelu>(cfg, dtype, a, s);
     case Epi::SwiGlu: return launch_role<R, Epi::SwiGlu>(cfg, dtype, a, s);
     case Epi::Attn: return launch_role<R, Epi::Attn>(cfg, dtype, a, s);
+    case Epi::Rope: return launch_role<R, Epi::Rope>(cfg, dtype, a, s);
     case Epi::DSwiGlu: return launch_role<R, Epi::DSwiGlu>(cfg, dtype, a, s);
   }
   return hipErrorInvalidValue;
@@ -866,6 +899,13 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     return ok ? launch_epi<R_QKV_FWD>(epi, C_P128x192, dtype, a, s) : hipErrorInvalidValue;
   }
   if (a.M < 0 || a.N <= 0 || a.K <= 0 || !a.A || !a.B || !a.out) return hipErrorInvalidValue;
+  // rotary epilogue: bf16 QKV projection without bias, 128-wide tiles holding
+  // whole heads of 64 or 128 columns, the pipelined kernel only (below)
+  const bool rope = epi == Epi::Rope;
+  if (rope && (dtype != DT_BF16 || role != R_QKV_FWD || a.bias || !a.rope_tab || a.rope_S <= 0 ||
+               (a.rope_dh != 64 && a.rope_dh != 128) || a.rope_cols % a.rope_dh || a.rope_cols > a.N ||
+               a.N % 128))
+    return hipErrorInvalidValue;
   if (a.M == 0) return hipSuccess;
   if (a.N % 4 || a.ldo % 4 || a.lda < a.K || a.ldb < a.K) return hipErrorInvalidValue;
   if ((epi == Epi::Resid || epi == Epi::DGelu || epi == Epi::DSwiGlu) && (!a.aux || a.ld_aux % 4))
@@ -889,13 +929,15 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     // two stages (two workgroups per CU) once there are two 128x128 tiles per CU
     const Cfg c128 = tiles(128, 128) >= 512 ? C_P128x128_2 : C_P128x128_3;
     if (a.K % 64 == 0 && al_epi && small_off) {
-      const bool glu = epi == Epi::SwiGlu || epi == Epi::DSwiGlu;
+      // the gated and rotary epilogues take only the 64-wide wave tiles
+      const bool glu = epi == Epi::SwiGlu || epi == Epi::DSwiGlu || rope;
       if (!glu && a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
       else if (!glu && a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
       else if (!glu && a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
       else if (a.K > 1024 && a.N % 128 == 0 && tiles(256, 128) >= 256) cfg = C_P256x128_8W;
       else cfg = c128;
     } else {
+      if (rope) return hipErrorInvalidValue;
       const long tiles128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
       cfg = tiles128 >= 512 ? C_REG_128x128 : C_REG_64x128;
     }

@@ -41,6 +41,9 @@ enum class Epi {
             // out2[m, f] = gate, out2[m, half + f] = up (if non-null)
   DSwiGlu,  // acc = d(act)[m, f]; aux = [gate | up]; out[m, f] = d gate,
             // out[m, half + f] = d up
+  Rope,     // bf16 QKV projection, no bias: out = acc with the rotary embedding
+            // applied to columns < rope_cols (Q and K, heads of rope_dh
+            // columns; row m is position m % rope_S)
   Attn,     // bf16 QKV projection with B rows in per-head order [Q_h K_h V_h]
             // (d_head 64) and M = sequences of 128 tokens: pre = acc + bias;
             // out = pre (if non-null); out2[:, 64h..64h+63] = softmax(Q_h K_h^T / 8) V_h
@@ -57,6 +60,9 @@ struct GemmArgs {
   void* out2; int ldo2;
   int half;
   float* lse;  // Attn only
+  // Rope only: (cos, sin) of pos * theta^(-2i/dh), [positions][rope_dh / 2]
+  const float2* rope_tab;
+  int rope_S, rope_dh, rope_cols;
 };
 
 // Names of the GEMM call sites (each gets its own kernel symbol).
@@ -74,6 +80,8 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
 struct AttnArgs {
   int B, S, H, dh;
   int causal, rope;
+  int rope_in_qkv;              // bf16, rope: Q and K in qkv are already rotated (no rotation on
+                                // load); dQ and dK are still rotated back on output
   float theta;
   const float2* rope_tab;       // rope: (cos, sin) of pos * theta^(-2i/dh), [rope_rows][dh/2]
   int rope_rows;                // positions the table covers (>= S)

@@ -493,6 +493,9 @@ struct Ctx {
   void* W(size_t off) const { return off == NONE ? nullptr : scratch + off; }
 };
 
+// bf16 pre-RMS stages rotate Q and K in the QKV projection's epilogue
+static bool rope_in_qkv(const Ctx& c) { return c.llama && c.dt == DT_BF16; }
+
 static ringada_status gemm(const Ctx& c, Role role, Epi epi, int M, int N, int K, const void* A, int lda,
                            const void* B, int ldb, void* out, int ldo, const void* bias = nullptr,
                            const void* aux = nullptr, int ld_aux = 0, void* out2 = nullptr, int ldo2 = 0,
@@ -547,14 +550,24 @@ static ringada_status block_forward(const Ctx& c, int l, const void* X, void* Y)
     RG_TRY(run(st, c.s, "gemm_qkv_attn_fwd", 2.0 * T * 3.0 * d * d + attn_flops, bytes,
                [&] { return launch_gemm(c.dt, R_QKV_FWD, Epi::Attn, g, c.s); }));
   } else {
-    RG_TRY(gemm(c, R_QKV_FWD, Epi::Store, T, 3 * d, d, xin, d, b.wt_qkv, d, qkv, 3 * d,
-                st->qkv_per_head ? b.bqkv : b.w.b_qkv));
+    if (rope_in_qkv(c)) {
+      // the rotary embedding applied once, in the projection's epilogue: the
+      // stash keeps the rotated Q and K, which the attention loads as they are
+      GemmArgs g{xin, d, b.wt_qkv, d, T, 3 * d, d, nullptr, nullptr, 0, qkv, 3 * d, nullptr, 0, 0};
+      g.rope_tab = st->rope_tab; g.rope_S = L.S; g.rope_dh = c.dh; g.rope_cols = 2 * d;
+      RG_TRY(run(st, c.s, role_name(R_QKV_FWD), 2.0 * T * 3.0 * d * d, es * ((double)T * d + 3.0 * d * d + 3.0 * T * d),
+                 [&] { return launch_gemm(c.dt, R_QKV_FWD, Epi::Rope, g, c.s); }));
+    } else {
+      RG_TRY(gemm(c, R_QKV_FWD, Epi::Store, T, 3 * d, d, xin, d, b.wt_qkv, d, qkv, 3 * d,
+                  st->qkv_per_head ? b.bqkv : b.w.b_qkv));
+    }
     AttnArgs aa{};
     aa.B = L.B; aa.S = L.S; aa.H = c.H; aa.dh = c.dh;
     aa.causal = c.llama; aa.rope = c.llama; aa.theta = st->D.rope_theta;
     aa.rope_tab = st->rope_tab; aa.rope_rows = st->D.max_seq;
     aa.qkv = qkv; aa.ld_qkv = 3 * d; aa.o = o; aa.ld_o = d; aa.lse = lse;
     if (st->qkv_per_head) { aa.qkv_hs = 3 * c.dh; aa.qkv_ko = c.dh; aa.qkv_vo = 2 * c.dh; }
+    aa.rope_in_qkv = rope_in_qkv(c);
     RG_TRY(run(st, c.s, "attn_fwd", attn_flops, es * 4.0 * T * d, [&] { return launch_attn_fwd(c.dt, aa, c.s); }));
   }
   RG_TRY(gemm(c, R_O_FWD, Epi::Store, T, d, d, o, d, b.wt_o, d, attn, d, b.w.b_o));
@@ -737,6 +750,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   at.rope_tab = st->rope_tab; at.rope_rows = st->D.max_seq;
   at.qkv = c.S(sb.qkv); at.ld_qkv = 3 * d; at.o = c.S(sb.o); at.ld_o = d;
   if (st->qkv_per_head) { at.qkv_hs = 3 * c.dh; at.qkv_ko = c.dh; at.qkv_vo = 2 * c.dh; }
+  at.rope_in_qkv = rope_in_qkv(c);
   at.lse = static_cast<float*>(c.S(sb.lse));
   at.dout = c.W(L.dout); at.ld_do = d; at.dsum = static_cast<float*>(c.W(L.dsum));
   at.dqkv = c.W(L.dqkv); at.ld_dqkv = 3 * d;
