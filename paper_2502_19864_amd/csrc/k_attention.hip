@@ -144,12 +144,20 @@ __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
 
   const int qlast = min(S - 1, qb * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
+  // the next K/V tile's global loads are in flight (in registers) while the
+  // current tile is computed on
+  TileLoad<DH, 64 * NW> tk, tv;
+  tk.issue(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, b, S, 0);
+  tv.issue(qkv, a.ld_qkv, a.qkv_vo + hd * a.qkv_hs, b, S, 0);
   for (int kt = 0; kt < nkt; ++kt) {
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, rot_load(a), sK, qkv, a.ld_qkv,
-                                a.qkv_vo + hd * a.qkv_hs, sV, b, S,
-                                kt * KT, rtab);
+    tk.store(sK, rot_load(a), S, kt * KT, rtab);
+    tv.store(sV, false, S, kt * KT, rtab);
     __syncthreads();
+    if (kt + 1 < nkt) {
+      tk.issue(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, b, S, (kt + 1) * KT);
+      tv.issue(qkv, a.ld_qkv, a.qkv_vo + hd * a.qkv_hs, b, S, (kt + 1) * KT);
+    }
     f32x16 sc[KT / 32];
 #pragma unroll
     for (int kb = 0; kb < KT / 32; ++kb) {
