@@ -268,14 +268,21 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 
   const int qlast = min(S - 1, qb * (32 * NW) + 32 * NW - 1);
   const int nkt = CAUSAL ? qlast / KT + 1 : (S + KT - 1) / KT;
+  // the next K/V tile's global loads are in flight while the current one is used
+  TileLoad<DH, 64 * NW> tk, tv;
+  tk.issue(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, b, S, 0);
+  tv.issue(qkv, a.ld_qkv, a.qkv_vo + hd * a.qkv_hs, b, S, 0);
   for (int kt = 0; kt < nkt; ++kt) {
     // every query of the workgroup and every key of the tile in range, no causal mask
     const bool full = !CAUSAL && (qb + 1) * (32 * NW) <= S && (kt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, rot_load(a), sK, qkv, a.ld_qkv,
-                                a.qkv_vo + hd * a.qkv_hs, sV, b, S,
-                                kt * KT, rtab);
+    tk.store(sK, rot_load(a), S, kt * KT, rtab);
+    tv.store(sV, false, S, kt * KT, rtab);
     __syncthreads();
+    if (kt + 1 < nkt) {
+      tk.issue(qkv, a.ld_qkv, a.qkv_ko + hd * a.qkv_hs, b, S, (kt + 1) * KT);
+      tv.issue(qkv, a.ld_qkv, a.qkv_vo + hd * a.qkv_hs, b, S, (kt + 1) * KT);
+    }
     // one key block at a time (not unrolled): keeps the kernel within the
     // registers of two waves per SIMD, so a (batch, head) grid fits one round
 #pragma unroll 1
@@ -340,16 +347,28 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
 
   const int nqt = (S + KT - 1) / KT;
   const int qt0 = CAUSAL ? (kb0 * (32 * NW)) / KT : 0;
+  // the next Q/dO tile's global loads are in flight while the current one is used
+  TileLoad<DH, 64 * NW> tq, tdo;
+  if (qt0 < nqt) {
+    tq.issue(qkv, a.ld_qkv, hd * a.qkv_hs, b, S, qt0 * KT);
+    tdo.issue(dO, a.ld_do, hd * DH, b, S, qt0 * KT);
+  }
   for (int qt = qt0; qt < nqt; ++qt) {
     // every key of the workgroup and every query of the tile in range, no causal mask
     const bool full = !CAUSAL && (kb0 + 1) * (32 * NW) <= S && (qt + 1) * KT <= S;
     __syncthreads();
-    load_tile_pair<DH, 64 * NW>(qkv, a.ld_qkv, hd * a.qkv_hs, rot_load(a), sQ, dO, a.ld_do, hd * DH, sO, b, S, qt * KT,
-                                rtab);
+    tq.store(sQ, rot_load(a), S, qt * KT, rtab);
+    tdo.store(sO, false, S, qt * KT, rtab);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
       sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
       sD[i] = qq < S ? a.dsum[(long)bh * S + qq] : 0.f;
+    }
+    // issued after the row statistics: loads complete in order, so waiting
+    // for those must not wait for the prefetch
+    if (qt + 1 < nqt) {
+      tq.issue(qkv, a.ld_qkv, hd * a.qkv_hs, b, S, (qt + 1) * KT);
+      tdo.issue(dO, a.ld_do, hd * DH, b, S, (qt + 1) * KT);
     }
     __syncthreads();
     // one query block at a time (not unrolled), as in the dQ pass
