@@ -366,10 +366,9 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
   static_assert(NS >= 2 && NS <= 4 && LPT * (NS - 1) < 64, "stages / vmcnt range");
   static_assert(E != Epi::SwiGlu || FN % 2 == 0, "SwiGlu needs gate/up block pairs");
   // output tile staging for the epilogue: fp32 rows of BN + 4 (the 16-B pad
-  // spreads the rows one fragment store touches over all banks), RPP rows
-  // (a multiple of 32)
-  // per pass through the stage buffers; the tile's bias columns (fp32) sit
-  // at the end of those buffers, past the staging rows
+  // spreads the rows one fragment store touches over all banks), RPP rows (a
+  // multiple of 32) per pass through the stage buffers; the tile's bias
+  // columns (fp32) sit at the end of those buffers, past the staging rows
   constexpr int CPF = BN + 4;
   constexpr bool HAS_BIAS = E == Epi::Store || E == Epi::Gelu || E == Epi::Attn;
   constexpr int BIASB = HAS_BIAS ? BN * 4 : 0;
