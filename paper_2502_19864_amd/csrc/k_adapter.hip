@@ -30,18 +30,22 @@ constexpr int GP = MB + 8;
 // the add + norm phase then runs one wave per token (NW == TOK), so the row
 // statistics are wave reductions and each lane handles features
 // 4*lane + 256*j, which makes every load and store of that phase one
-// contiguous 512-B run per instruction.
+// contiguous 512-B run per instruction.  The down projection's k-slice
+// partial sums go through LDS unit-major, [slice][unit][token] with a token
+// stride of 17 floats: the MFMA writes (16 tokens of 4 units per lane group)
+// and the GELU phase's reads (one unit per lane) spread over the banks,
+// where 64-float token rows put the 16 tokens of a lane group on one bank.
 template <int FB>
 __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
-  constexpr int NW = 16, KS = 4;
+  constexpr int NW = 16, KS = 4, TOKP = 17;
   constexpr int D = 256 * FB, DP = D + 8, VP = D + 4;
   constexpr int SLICE = D / KS, NSTEP = SLICE / 32;
   static_assert(NW == TOK, "one wave per token in the norm phase");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* sZ = reinterpret_cast<bf16*>(smem);                // [TOK][DP]
   bf16* sG = sZ + TOK * DP;                                // [TOK][GP]
-  float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][TOK][MB]
-  float* sV = sUp + KS * TOK * MB;                         // [TOK][VP]
+  float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][MB][TOKP]
+  float* sV = sUp + KS * MB * TOKP;                        // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T, t0 = blockIdx.x * TOK;
   const bf16* z = static_cast<const bf16*>(a.z);
@@ -97,20 +101,15 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 #pragma unroll
     for (int j = 0; j < NSTEP; ++j) u = mfma16(wd[j], ld_frag(zr + j * 32), u);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) sUp[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = u[r];
+    for (int r = 0; r < 4; ++r) sUp[(ks * MB + ug * 16 + 4 * grp + r) * TOKP + l16] = u[r];
     __syncthreads();
-    if (ks == 0) {
-      float uv[4], gv[4];
+    {  // one (token, unit) pair per thread: sum of the k slices, GELU
+      const int unit = lane, tok = wave;
+      float sum = 0.f;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        float s = 0.f;
-#pragma unroll
-        for (int k2 = 0; k2 < KS; ++k2) s += sUp[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
-        uv[r] = s;
-        gv[r] = gelu_fast(s);
-      }
-      if (a.u && t0 + l16 < T) St<bf16>::st4(static_cast<bf16*>(a.u), (long)(t0 + l16) * MB + ug * 16 + 4 * grp, uv);
-      St<bf16>::st4(sG, l16 * GP + ug * 16 + 4 * grp, gv);
+      for (int k2 = 0; k2 < KS; ++k2) sum += sUp[(k2 * MB + unit) * TOKP + tok];
+      if (a.u && t0 + tok < T) static_cast<bf16*>(a.u)[(long)(t0 + tok) * MB + unit] = f2bf(sum);
+      sG[tok * GP + unit] = f2bf(gelu_fast(sum));
     }
     __syncthreads();
   }
@@ -195,25 +194,23 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 //     contiguous 512-B run per instruction and the row sums are wave
 //     reductions; dz stays in fp32 registers and goes to LDS (bf16) for
 //     2. dV = dZ W_up^T (k split over 4 waves, MFMA, lane = token), dU =
-//     dV * gelu'(U);
+//     dV * gelu'(U) with one (token, unit) pair per thread;
 //  3. dU W_down^T (MFMA), staged in LDS as fp32, then dzin = dz + that, again
 //     one wave per token.
 // Every weight fragment is loaded while the previous phase runs.
 template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
-  constexpr int KS = NW / 4;
+  constexpr int KS = NW / 4, TOKP = TOK + 1;
   constexpr int D = 16 * NW * FB, DP = D + 8, VP = D + 4, SLICE = D / KS;
   static_assert(NW == TOK, "one wave per token in the row phases");
   static_assert(D == 256 * FB, "four consecutive features per lane, FB runs of 256");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
   bf16* sdZ = reinterpret_cast<bf16*>(smem);                       // [TOK][DP]
   bf16* sdU = sdZ + TOK * DP;                                      // [TOK][GP]
-  float* sPart = reinterpret_cast<float*>(sdU + TOK * GP);         // [KS][TOK][MB]
-  float* sV = sPart + KS * TOK * MB;                               // [TOK][VP]
+  float* sPart = reinterpret_cast<float*>(sdU + TOK * GP);         // [KS][MB][TOKP]
+  float* sV = sPart + KS * MB * TOKP;                              // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T;
-  const int token = blockIdx.x * TOK + l16;  // this lane's token in the MFMA phases
-  const bool tv = token < T;
   const int tw = blockIdx.x * TOK + wave;    // this wave's token in the row phases
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
@@ -228,10 +225,9 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 #pragma unroll
     for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
   }
-  // pre-activation of this lane's four units (read in the dV phase), loaded now
-  const int ug0 = (wave % 4) * 16 + 4 * grp;
-  uint2 uraw = make_uint2(0, 0);
-  if (has_ad && tv && wave < 4) uraw = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.u) + (long)token * MB + ug0);
+  // pre-activation of unit `lane` of this wave's token (read in the dU phase), loaded now
+  bf16 uraw = f2bf(0.f);
+  if (has_ad && twv) uraw = static_cast<const bf16*>(a.u)[(long)tw * MB + lane];
 
   // ---- gradient at the adapter output, one wave per token (features 4 lane + 256 j)
   float dz[FB][4];
@@ -293,36 +289,25 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   }
   __syncthreads();
 
-  // ---- dV^T[unit][token] = W_up[unit][:] . dZ[token][:]; dU = dV * gelu'(U)
+  // ---- dV^T[unit][token] = W_up[unit][:] . dZ[token][:], k split over KS waves; the
+  // slices' partial sums go through LDS unit-major (token stride 17 floats, so the
+  // MFMA writes and the one-unit-per-lane reads spread over the banks); then
+  // dU = dV * gelu'(U) with one (token, unit) pair per thread
   {
     const bf16* zr = sdZ + l16 * DP + ks * SLICE + 8 * grp;
-    const int j0 = ug * 16 + 4 * grp;
-    const float uu[4] = {__uint_as_float(uraw.x << 16), __uint_as_float(uraw.x & 0xffff0000u),
-                         __uint_as_float(uraw.y << 16), __uint_as_float(uraw.y & 0xffff0000u)};
     f32x4 dv = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
     for (int j = 0; j < NSTEP; ++j) dv = mfma16(wup_f[j], ld_frag(zr + j * 32), dv);
-    if constexpr (KS > 1) {
 #pragma unroll
-      for (int r = 0; r < 4; ++r) sPart[(ks * TOK + l16) * MB + ug * 16 + 4 * grp + r] = dv[r];
-      __syncthreads();
-      if (ks == 0) {
+    for (int r = 0; r < 4; ++r) sPart[(ks * MB + ug * 16 + 4 * grp + r) * TOKP + l16] = dv[r];
+    __syncthreads();
+    const int unit = lane;
+    float sum = 0.f;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          float sum = 0.f;
-#pragma unroll
-          for (int k2 = 0; k2 < KS; ++k2) sum += sPart[(k2 * TOK + l16) * MB + ug * 16 + 4 * grp + r];
-          dv[r] = sum;
-        }
-      }
-    }
-    if (ks == 0) {
-      float du[4];
-#pragma unroll
-      for (int r = 0; r < 4; ++r) du[r] = dv[r] * gelu_grad_fast(uu[r]);
-      if (tv) St<bf16>::st4(static_cast<bf16*>(a.du), (long)token * MB + j0, du);
-      St<bf16>::st4(sdU, (long)l16 * GP + j0, du);
-    }
+    for (int k2 = 0; k2 < KS; ++k2) sum += sPart[(k2 * MB + unit) * TOKP + wave];
+    const bf16 du = f2bf(sum * gelu_grad_fast(bf2f(uraw)));
+    if (twv) static_cast<bf16*>(a.du)[(long)tw * MB + unit] = du;
+    sdU[wave * GP + unit] = du;
   }
   if (!a.dzin) return;
   __syncthreads();
@@ -703,7 +688,7 @@ static bool bf16_shape(int d, int& nw, int& fb) {
 template <int FB>
 static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
   constexpr int D = 256 * FB;
-  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)4 * TOK * MB * 4 +
+  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)4 * MB * (TOK + 1) * 4 +
                     (size_t)TOK * (D + 4) * 4;
   static bool attr = false;
   if (!attr) {
@@ -719,7 +704,7 @@ static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
 template <int NW, int FB>
 static hipError_t bwd_k(const AdapterBwdArgs& a, hipStream_t s) {
   constexpr int D = 16 * NW * FB;
-  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * TOK * MB * 4 +
+  const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)(NW / 4) * (TOK + 1) * MB * 4 +
                     (size_t)TOK * (D + 4) * 4;
   static bool attr = false;
   if (!attr) {
