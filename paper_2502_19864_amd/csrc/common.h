@@ -176,6 +176,24 @@ __device__ __forceinline__ const bf16* pack_b_frag(const void* base, int d, int 
   return static_cast<const bf16*>(base) + ((long)(wave * 2 * (d / 256) + 2 * b + h) * 64 + lane) * 8;
 }
 
+// ---------------------------------------------------------------- global -> LDS DMA
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+// Global -> LDS DMA, 16 B per lane (lane i lands at the LDS address + 16 i),
+// issued from inline assembly: scalar base + 32-bit per-lane byte
+// offset, LDS destination (wave-uniform byte address) in M0.  The compiler's
+// wait-count pass does not see these loads, so it inserts no vmcnt waits of
+// its own before LDS reads; the kernel waits for them explicitly (vmcnt
+// counts them like any vector load).  Kernels using this touch M0 nowhere
+// else.
+__device__ __forceinline__ void dma16_m0(const void* gbase, uint32_t voff, uint32_t lds) {
+  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(gbase)
+               : "memory");
+}
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_ptr_t)p;
+}
+
 // ---------------------------------------------------------------- XCD-aware block order
 // Workgroups are dispatched round-robin over the 8 XCDs (linear workgroup id i
 // runs on XCD i % 8), each XCD with its own L2.  xcd_block maps the linear id

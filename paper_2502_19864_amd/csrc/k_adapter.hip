@@ -47,17 +47,25 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][MB][TOKP]
   float* sV = sUp + KS * MB * TOKP;                        // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
-  const int T = a.T, t0 = blockIdx.x * TOK;
+  const int T = a.T, t0 = xcd_block(blockIdx.x, gridDim.x) * TOK;
   const bf16* z = static_cast<const bf16*>(a.z);
 
-  // ---- every global load up front
-  constexpr int CPR = D / 8, NCH = TOK * CPR, PER = (NCH + 1023) / 1024;
-  uint4 zv[PER];
+  // ---- every global load up front.  The z tile goes by DMA straight into its padded LDS
+  // rows: 16-B slot s is chunk s % SPR of row s / SPR, the row's last slot is padding; the
+  // slots past the tile land in the sG / sUp space, which is written only after the wait.
+  // Slots with no data (padding, rows past T) load the tile's first chunk instead.
+  constexpr int SPR = DP / 8, NSLOT = TOK * SPR, NI = (NSLOT + 1023) / 1024;
+  static_assert(NI * 1024 * 16 <= (TOK * DP + TOK * GP) * 2 + KS * MB * TOKP * 4,
+                "the DMA's spare slots stay clear of sV");
+  {
+    const bf16* zb = z + (long)t0 * D;
 #pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = threadIdx.x + i * 1024, r = c / CPR, k = (c % CPR) * 8;
-    zv[i] = (c < NCH && t0 + r < T) ? *reinterpret_cast<const uint4*>(z + (long)(t0 + r) * D + k)
-                                    : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < NI; ++i) {
+      const int sl = (i * NW + wave) * 64 + lane, r = sl / SPR, c = sl % SPR;
+      const bool ok = sl < NSLOT && c < D / 8 && t0 + r < T;
+      dma16_m0(zb, ok ? (uint32_t)((r * D + 8 * c) * 2) : 0u,
+               lds_addr(sZ) + (uint32_t)__builtin_amdgcn_readfirstlane((i * NW + wave) * 1024));
+    }
   }
   const bool has_ad = a.wdn_t != nullptr;  // else: residual add + norm only
   const int ug = wave % 4, ks = wave / 4;
@@ -78,20 +86,25 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   const int tw = t0 + wave;  // this wave's token in the norm phase
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
+  // the norm's affine parameters, loaded with everything else rather than after the last
+  // barrier, and the residual row last: it is needed last.  No load here is conditional
+  // (an absent gamma / beta reads z's first row instead, a row past T row 0), so the
+  // compiler's wait counts stay exact and the weight fragments are not waited for along
+  // with the residual.
+  const bf16* gp = static_cast<const bf16*>(a.norm != Norm::None ? a.gamma : a.z);
+  const bf16* bp = static_cast<const bf16*>(a.norm == Norm::LN ? a.beta : a.z);
   uint2 rr[FB], gmv[FB], btv[FB];
 #pragma unroll
   for (int j = 0; j < FB; ++j) {
     const int f = 4 * lane + 256 * j;
-    rr[j] = twv ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + f) : make_uint2(0, 0);
-    // the norm's affine parameters, loaded with everything else rather than after the last barrier
-    gmv[j] = a.norm != Norm::None ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.gamma) + f) : make_uint2(0, 0);
-    btv[j] = a.norm == Norm::LN ? *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.beta) + f) : make_uint2(0, 0);
+    gmv[j] = *reinterpret_cast<const uint2*>(gp + f);
+    btv[j] = *reinterpret_cast<const uint2*>(bp + f);
+    rr[j] = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + f);
   }
-#pragma unroll
-  for (int i = 0; i < PER; ++i) {
-    const int c = threadIdx.x + i * 1024, r = c / CPR, k = (c % CPR) * 8;
-    if (c < NCH) *reinterpret_cast<uint4*>(sZ + r * DP + k) = zv[i];
-  }
+  // the z tile has landed once no more than the weight-fragment loads issued after it are
+  // pending (vmcnt counts in issue order)
+  if (has_ad) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NSTEP + 2 * FB) : "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   __syncthreads();
 
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:], k split over KS waves
@@ -177,8 +190,9 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
     float xh[4], o[4];
     const float gm[4] = {__uint_as_float(gmv[j].x << 16), __uint_as_float(gmv[j].x & 0xffff0000u),
                          __uint_as_float(gmv[j].y << 16), __uint_as_float(gmv[j].y & 0xffff0000u)};
-    const float bt[4] = {__uint_as_float(btv[j].x << 16), __uint_as_float(btv[j].x & 0xffff0000u),
-                         __uint_as_float(btv[j].y << 16), __uint_as_float(btv[j].y & 0xffff0000u)};
+    const uint2 bq = a.norm == Norm::LN ? btv[j] : make_uint2(0, 0);  // RMSNorm has no shift
+    const float bt[4] = {__uint_as_float(bq.x << 16), __uint_as_float(bq.x & 0xffff0000u),
+                         __uint_as_float(bq.y << 16), __uint_as_float(bq.y & 0xffff0000u)};
 #pragma unroll
     for (int q = 0; q < 4; ++q) xh[q] = (v[j][q] - mean) * rstd;
 #pragma unroll
@@ -211,7 +225,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   float* sV = sPart + KS * MB * TOKP;                              // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T;
-  const int tw = blockIdx.x * TOK + wave;    // this wave's token in the row phases
+  const int tw = xcd_block(blockIdx.x, gridDim.x) * TOK + wave;  // this wave's token in the row phases
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
 

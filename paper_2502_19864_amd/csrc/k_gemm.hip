@@ -296,8 +296,6 @@ __device__ __forceinline__ void tile_coords(int M, int N, int& m0, int& n0) {
   n0 = (r / gsize) * BN;
 }
 
-typedef __attribute__((address_space(3))) void* lds_ptr_t;
-
 // Scheduling hint for one k-step of the pipelined kernel: alternate one LDS
 // fragment read (of the next k-step) with one MFMA (of this one), ND reads in
 // all, so the reads drain while the matrix core works instead of bunching up
@@ -308,21 +306,6 @@ __device__ __forceinline__ void interleave_ds_mfma(std::integer_sequence<int, Q.
     if constexpr (Q < ND) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);  // DS read
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                        // MFMA
   }(), ...);
-}
-
-// Global -> LDS DMA, 16 B per lane (lane i lands at the LDS address + 16 i),
-// issued from inline assembly: scalar base + 32-bit per-lane byte
-// offset, LDS destination (wave-uniform byte address) in M0.  The compiler's
-// wait-count pass does not see these loads, so it inserts no vmcnt waits of
-// its own before LDS reads; the kernel waits for them explicitly (vmcnt
-// counts them like any vector load).  Kernels using this touch M0 nowhere
-// else.
-__device__ __forceinline__ void dma16_m0(const void* gbase, uint32_t voff, uint32_t lds) {
-  asm volatile("s_mov_b32 m0, %0\n\ts_nop 0\n\tglobal_load_lds_dwordx4 %1, %2" ::"s"(lds), "v"(voff), "s"(gbase)
-               : "memory");
-}
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return (uint32_t)(uintptr_t)(lds_ptr_t)p;
 }
 
 template <int N>
