@@ -211,7 +211,9 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
 //     dV * gelu'(U) with one (token, unit) pair per thread;
 //  3. dU W_down^T (MFMA), staged in LDS as fp32, then dzin = dz + that, again
 //     one wave per token.
-// Every weight fragment is loaded while the previous phase runs.
+// Every global load the kernel makes is issued before the first phase, the
+// weight fragments of both contractions first (at d = 1024 those of W_down
+// after the norm backward, for want of registers).
 template <int NW, int FB>
 __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   constexpr int KS = NW / 4, TOKP = TOK + 1;
@@ -229,60 +231,92 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
 
-  // fragments of W_up for the first contraction: in flight during the norm backward
+  // ---- every global load up front: the weight fragments of both contractions, then the
+  // pre-activation, the norm backward's rows and its parameters.  None of the row loads
+  // is conditional (a row past T reads row 0, an operand the norm does not have reads
+  // gin instead), so no load waits for the one before it and the compiler's wait counts
+  // stay exact; the values are unpacked only once everything is in flight.
   const int ug = wave % 4, ks = wave / 4;
   constexpr int NSTEP = SLICE / 32;
   static_assert(FB <= 4, "d <= 1024: every weight fragment fits the registers (wider widths split the work)");
   const bool has_ad = a.wup != nullptr;  // else: the norm backward only
-  bf16x8 wup_f[NSTEP];
+  const int f0 = wave * 16 * FB;
+  // at d = 1024 the W_down fragments would not fit the registers beside the rows (the
+  // kernel spilled): there they are loaded after the norm backward, during the dV phase
+  constexpr bool EARLY_WDN = FB <= 3;
+  bf16x8 wup_f[NSTEP], w0[FB], w1[FB];
+  auto load_wdn = [&] {
+#pragma unroll
+    for (int b = 0; b < FB; ++b) {
+      w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
+      w1[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 1, lane));
+    }
+  };
   if (has_ad) {
 #pragma unroll
     for (int j = 0; j < NSTEP; ++j) wup_f[j] = ld_frag(pack_a_frag(a.wup, D, wave, j, lane));
+    if constexpr (EARLY_WDN)
+      if (a.dzin) load_wdn();
   }
-  // pre-activation of unit `lane` of this wave's token (read in the dU phase), loaded now
-  bf16 uraw = f2bf(0.f);
-  if (has_ad && twv) uraw = static_cast<const bf16*>(a.u)[(long)tw * MB + lane];
+  const bf16* gin = static_cast<const bf16*>(a.gin);
+  // pre-activation of unit `lane` of this wave's token (read in the dU phase)
+  const bf16 uraw = (has_ad ? static_cast<const bf16*>(a.u) : gin)[(long)(twv ? tw : 0) * MB + lane];
+  const bf16* xp = a.norm != Norm::None ? static_cast<const bf16*>(a.xhat) : gin;
+  const bf16* dp = a.norm == Norm::RMS ? static_cast<const bf16*>(a.dres) : gin;
+  const bf16* gp = a.norm != Norm::None ? static_cast<const bf16*>(a.gamma) : gin;
+  const float* rp = a.norm != Norm::None ? a.rstd : reinterpret_cast<const float*>(gin);
+  uint2 rg[FB], rx[FB], rd[FB], rm[FB];
+#pragma unroll
+  for (int j = 0; j < FB; ++j) {
+    const int f = 4 * lane + 256 * j;
+    rg[j] = *reinterpret_cast<const uint2*>(gin + wrow + f);
+    rx[j] = *reinterpret_cast<const uint2*>(xp + wrow + f);
+    rd[j] = *reinterpret_cast<const uint2*>(dp + wrow + f);
+    rm[j] = *reinterpret_cast<const uint2*>(gp + f);
+  }
+  const float rsv = rp[twv ? tw : 0];
 
   // ---- gradient at the adapter output, one wave per token (features 4 lane + 256 j)
+  auto unpack = [](uint2 q, float v[4]) {
+    v[0] = __uint_as_float(q.x << 16); v[1] = __uint_as_float(q.x & 0xffff0000u);
+    v[2] = __uint_as_float(q.y << 16); v[3] = __uint_as_float(q.y & 0xffff0000u);
+  };
   float dz[FB][4];
   {
     float gg[FB][4], xh[FB][4], dr[FB][4], gm[FB][4];
 #pragma unroll
     for (int j = 0; j < FB; ++j) {
-      const int f = 4 * lane + 256 * j;
+      unpack(rg[j], gg[j]);
+      unpack(rx[j], xh[j]);
+      unpack(rd[j], dr[j]);
+      unpack(rm[j], gm[j]);
 #pragma unroll
-      for (int q = 0; q < 4; ++q) gg[j][q] = xh[j][q] = dr[j][q] = gm[j][q] = 0.f;
-      if (twv) {
-        St<bf16>::ld4(static_cast<const bf16*>(a.gin), wrow + f, gg[j]);
-        if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.xhat), wrow + f, xh[j]);
-        if (a.norm == Norm::RMS) St<bf16>::ld4(static_cast<const bf16*>(a.dres), wrow + f, dr[j]);
+      for (int q = 0; q < 4; ++q)
+        if (!twv || a.norm != Norm::RMS) dr[j][q] = 0.f;
+    }
+    // one formula for every norm (no branch the compiler could sink the loads into);
+    // without a norm dz is gin itself
+    const bool none = a.norm == Norm::None;
+    const float rs = (twv && !none) ? rsv : 0.f;
+    float s1 = 0.f, s2 = 0.f;
+#pragma unroll
+    for (int j = 0; j < FB; ++j)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const float g = gg[j][q] * gm[j][q];
+        s1 += g;
+        s2 += g * xh[j][q];
       }
-      if (a.norm != Norm::None) St<bf16>::ld4(static_cast<const bf16*>(a.gamma), f, gm[j]);
-    }
-    const float rs = (twv && a.norm != Norm::None) ? a.rstd[tw] : 0.f;
-    if (a.norm == Norm::None) {
+    constexpr float inv_d = 1.f / (float)D;
+    const float m1 = (a.norm == Norm::LN) ? wave_sum(s1) * inv_d : 0.f;
+    const float m2 = wave_sum(s2) * inv_d;
 #pragma unroll
-      for (int j = 0; j < FB; ++j)
+    for (int j = 0; j < FB; ++j)
 #pragma unroll
-        for (int q = 0; q < 4; ++q) dz[j][q] = gg[j][q];
-    } else {
-      float s1 = 0.f, s2 = 0.f;
-#pragma unroll
-      for (int j = 0; j < FB; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          gg[j][q] *= gm[j][q];
-          s1 += gg[j][q];
-          s2 += gg[j][q] * xh[j][q];
-        }
-      constexpr float inv_d = 1.f / (float)D;
-      const float m1 = (a.norm == Norm::LN) ? wave_sum(s1) * inv_d : 0.f;
-      const float m2 = wave_sum(s2) * inv_d;
-#pragma unroll
-      for (int j = 0; j < FB; ++j)
-#pragma unroll
-        for (int q = 0; q < 4; ++q) dz[j][q] = dr[j][q] + rs * (gg[j][q] - m1 - xh[j][q] * m2);
-    }
+      for (int q = 0; q < 4; ++q) {
+        const float v = dr[j][q] + rs * (gg[j][q] * gm[j][q] - m1 - xh[j][q] * m2);
+        dz[j][q] = none ? (twv ? gg[j][q] : 0.f) : v;
+      }
   }
 #pragma unroll
   for (int j = 0; j < FB; ++j) {
@@ -291,16 +325,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     St<bf16>::st4(sdZ, (long)wave * DP + f, dz[j]);
   }
   if (!has_ad) return;
-  // W_down fragments of the last contraction, in flight during the dV one
-  const int f0 = wave * 16 * FB;
-  bf16x8 w0[FB], w1[FB];
-  if (a.dzin) {
-#pragma unroll
-    for (int b = 0; b < FB; ++b) {
-      w0[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 0, lane));
-      w1[b] = ld_frag(pack_b_frag(a.wdn, D, wave, b, 1, lane));
-    }
-  }
+  if constexpr (!EARLY_WDN)
+    if (a.dzin) load_wdn();
   __syncthreads();
 
   // ---- dV^T[unit][token] = W_up[unit][:] . dZ[token][:], k split over KS waves; the
