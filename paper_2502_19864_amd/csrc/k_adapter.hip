@@ -482,21 +482,24 @@ __global__ __launch_bounds__(256) void adapter_wide_down(const bf16* X, const bf
   const bool tv = token < T;
   constexpr int NB = WIDE_KC / 4 / 32;  // 32-feature blocks per wave
   const int fb0 = (kc * WIDE_KC + wave * (WIDE_KC / 4)) / 32;
+  // every load issued before the first MFMA, none conditional (a token past T reads row 0;
+  // its column of the result is never stored)
   const bf16* xr = X + (long)(tv ? token : 0) * d + fb0 * 32 + 8 * grp;
-  bf16x8 xf[NB];
+  bf16x8 xf[NB], w[NB][4];
 #pragma unroll
-  for (int j = 0; j < NB; ++j) xf[j] = tv ? ld_frag(xr + j * 32) : zero_frag();
+  for (int j = 0; j < NB; ++j) xf[j] = ld_frag(xr + j * 32);
+#pragma unroll
+  for (int j = 0; j < NB; ++j)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) w[j][g] = ld_frag(pack_a_block(Wa, d, g, fb0 + j, lane));
+  __builtin_amdgcn_sched_barrier(0);  // keeps the scheduler from moving loads down to their MFMAs
   f32x4 acc[4];
 #pragma unroll
   for (int g = 0; g < 4; ++g) acc[g] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int j = 0; j < NB; ++j) {
-    bf16x8 w[4];
+  for (int j = 0; j < NB; ++j)
 #pragma unroll
-    for (int g = 0; g < 4; ++g) w[g] = ld_frag(pack_a_block(Wa, d, g, fb0 + j, lane));
-#pragma unroll
-    for (int g = 0; g < 4; ++g) acc[g] = mfma16(w[g], xf[j], acc[g]);
-  }
+    for (int g = 0; g < 4; ++g) acc[g] = mfma16(w[j][g], xf[j], acc[g]);
   // D[unit 16g + 4*grp + r][token l16]; the four waves' feature quarters summed in LDS
 #pragma unroll
   for (int g = 0; g < 4; ++g)
@@ -521,13 +524,52 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
   __shared__ __attribute__((aligned(16))) bf16 sG[TOK * GP];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int t0 = blockIdx.x * TOK, fc = blockIdx.y;
-  for (int i = threadIdx.x; i < TOK * MB; i += 256) {
-    const int tok = i / MB, j = i % MB, t = t0 + tok;
+  // Every load is issued before the first use: the split-K partial sums (four chunks per
+  // batch, chunk and token clamped, masked after the load), the pre-activation, then the
+  // weight fragments and the Z / R rows of the up projection.  None is conditional on a
+  // lane, so no load waits for the one before it.
+  constexpr int NIT = TOK * MB / 256, KB = 4;
+  float part[NIT][KB];
+  bf16 uiv[NIT];
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int i = threadIdx.x + it * 256, tok = i / MB, j = i % MB, t = min(t0 + tok, T - 1);
+#pragma unroll
+    for (int q = 0; q < KB; ++q) part[it][q] = P[((long)min(q, nkc - 1) * T + t) * MB + j];
+    uiv[it] = BWD ? ui[(long)t * MB + j] : f2bf(0.f);
+  }
+  const int token = t0 + l16;
+  const bool tv = token < T;
+  const long row = (long)(tv ? token : 0) * d;
+  constexpr int NBK = WIDE_UC / 16 / 4;  // 16-feature blocks per wave
+  const int b0 = (fc * WIDE_UC + wave * (WIDE_UC / 4)) / 16;
+  bf16x8 w[NBK][2];
+  uint2 zr[NBK], rr[NBK];
+  if (Wb) {
+#pragma unroll
+    for (int b = 0; b < NBK; ++b) {
+      w[b][0] = ld_frag(Wb + ((long)(2 * (b0 + b)) * 64 + lane) * 8);
+      w[b][1] = ld_frag(Wb + ((long)(2 * (b0 + b) + 1) * 64 + lane) * 8);
+    }
+    const bf16* Rp = R ? R : Z;
+#pragma unroll
+    for (int b = 0; b < NBK; ++b) {
+      const int f = (b0 + b) * 16 + 4 * grp;
+      zr[b] = *reinterpret_cast<const uint2*>(Z + row + f);
+      const uint2 rv = *reinterpret_cast<const uint2*>(Rp + row + f);
+      rr[b] = R ? rv : make_uint2(0, 0);
+    }
+  }
+#pragma unroll
+  for (int it = 0; it < NIT; ++it) {
+    const int i = threadIdx.x + it * 256, tok = i / MB, j = i % MB, t = t0 + tok;
     float sum = 0.f, g = 0.f;
+#pragma unroll
+    for (int q = 0; q < KB; ++q) sum += q < nkc ? part[it][q] : 0.f;
+    for (int kc = KB; kc < nkc; ++kc) sum += P[((long)kc * T + min(t, T - 1)) * MB + j];  // d > 4096 only
     if (t < T) {
-      for (int kc = 0; kc < nkc; ++kc) sum += P[((long)kc * T + t) * MB + j];
       if constexpr (BWD) {
-        g = sum * gelu_grad_fast(bf2f(ui[(long)t * MB + j]));
+        g = sum * gelu_grad_fast(bf2f(uiv[it]));
         if (fc == 0) uo[(long)t * MB + j] = f2bf(g);
       } else {
         g = gelu_fast(sum);
@@ -539,24 +581,6 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
   if (!Wb) return;
   __syncthreads();
   const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
-  const int token = t0 + l16;
-  const bool tv = token < T;
-  const long row = (long)(tv ? token : 0) * d;
-  constexpr int NBK = WIDE_UC / 16 / 4;  // 16-feature blocks per wave
-  const int b0 = (fc * WIDE_UC + wave * (WIDE_UC / 4)) / 16;
-  bf16x8 w[NBK][2];
-#pragma unroll
-  for (int b = 0; b < NBK; ++b) {
-    w[b][0] = ld_frag(Wb + ((long)(2 * (b0 + b)) * 64 + lane) * 8);
-    w[b][1] = ld_frag(Wb + ((long)(2 * (b0 + b) + 1) * 64 + lane) * 8);
-  }
-  uint2 zr[NBK], rr[NBK];
-#pragma unroll
-  for (int b = 0; b < NBK; ++b) {
-    const int f = (b0 + b) * 16 + 4 * grp;
-    zr[b] = tv ? *reinterpret_cast<const uint2*>(Z + row + f) : make_uint2(0, 0);
-    rr[b] = (tv && R) ? *reinterpret_cast<const uint2*>(R + row + f) : make_uint2(0, 0);
-  }
 #pragma unroll
   for (int b = 0; b < NBK; ++b) {
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};

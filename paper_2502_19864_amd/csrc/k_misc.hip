@@ -399,8 +399,12 @@ constexpr int HEAD_SPW = 4;  // samples per workgroup (one wave each)
 // workgroups zero rows 1..S-1 of every sequence with 16-B stores.
 template <typename T, int CN>  // CN: class count bound, compile time (the loops over classes unroll)
 __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh, const float* bh,
-                                                 int C, const int* labels, T* dy, float* gwh, float* gbh,
+                                                 int C_, const int* labels, T* dy, float* gwh, float* gbh,
                                                  float* loss) {
+  // the two-class instantiation runs only with C == 2: a compile-time class count leaves
+  // no class guard around a load, so the loads of a row go out together instead of one
+  // after the other
+  const int C = CN == 2 ? 2 : C_;
   const int nce = (B + HEAD_SPW - 1) / HEAD_SPW;
   if ((int)blockIdx.x >= nce) {
     const int nz = gridDim.x - nce, z = blockIdx.x - nce;
@@ -492,7 +496,10 @@ __global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d
       acc[c] = 0.f;
     }
 #pragma unroll
-    for (int s = 0; s < HEAD_SPW; ++s) yi[s] = s < ns ? St<T>::ld(y, (long)(j0 + s) * S * d + i) : 0.f;
+    for (int s = 0; s < HEAD_SPW; ++s) {  // unconditional load (sample clamped), masked after
+      const float v = St<T>::ld(y, (long)(j0 + min(s, ns - 1)) * S * d + i);
+      yi[s] = s < ns ? v : 0.f;
+    }
 #pragma unroll
     for (int s = 0; s < HEAD_SPW; ++s) {
       if (s >= ns) break;
