@@ -36,14 +36,12 @@ struct TileLoad {
 #pragma unroll
     for (int it = 0; it < IT; ++it) {
       const int p = threadIdx.x + it * NT;
-      const int r = p / HC, c = p % HC, row = r0 + r;
-      if (row < S) {
-        const bf16* a0 = src + (long)(b * S + row) * ld + col + c * 8;
-        raw[it][0] = ld_frag(a0);
-        raw[it][1] = ld_frag(a0 + DH / 2);
-      } else {
-        raw[it][0] = raw[it][1] = zero_frag();
-      }
+      // rows past S read row S - 1 and are zeroed in store(): no load is conditional on
+      // a lane, so none waits for the one before it
+      const int r = p / HC, c = p % HC, row = min(r0 + r, S - 1);
+      const bf16* a0 = src + (long)(b * S + row) * ld + col + c * 8;
+      raw[it][0] = ld_frag(a0);
+      raw[it][1] = ld_frag(a0 + DH / 2);
     }
   }
   __device__ __forceinline__ void store(bf16* dst, bool rot, int S, int r0, const float2* rtab) {
@@ -51,6 +49,7 @@ struct TileLoad {
     for (int it = 0; it < IT; ++it) {
       const int p = threadIdx.x + it * NT;
       const int r = p / HC, c = p % HC, row = r0 + r;
+      if (row >= S) raw[it][0] = raw[it][1] = zero_frag();
       if (rot && row < S) {
         float x1[8], x2[8];
         unpack_frag(raw[it][0], x1);
@@ -93,13 +92,17 @@ __device__ __forceinline__ bool rot_load(const AttnArgs& a) { return a.rope && !
 template <int DH>
 __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool valid, bool rot,
                                                const float2* rtab, int half, bf16x8 f[DH / 16]) {
+  // src is a valid row even when !valid (callers clamp it): the loads are unconditional
+  // and issued together, the values masked afterwards
   float x[DH / 16][8];
+  bf16x8 raw[DH / 16];
+#pragma unroll
+  for (int s = 0; s < DH / 16; ++s) raw[s] = ld_frag(src + 16 * s + 8 * half);
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
-    if (valid) unpack_frag(ld_frag(src + 16 * s + 8 * half), x[s]);
-    else
+    unpack_frag(raw[s], x[s]);
 #pragma unroll
-      for (int v = 0; v < 8; ++v) x[s][v] = 0.f;
+    for (int v = 0; v < 8; ++v) x[s][v] = valid ? x[s][v] : 0.f;
   }
   if (rot && valid) {
 #pragma unroll
@@ -245,19 +248,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   float dsum = 0.f;
   {
     const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
+    bf16x8 oraw[DH / 16];  // qrow is clamped: unconditional loads, masked after
+#pragma unroll
+    for (int s = 0; s < DH / 16; ++s) oraw[s] = ld_frag(orow + 16 * s + 8 * half);
 #pragma unroll
     for (int s = 0; s < DH / 16; ++s) {
       float ov[8], dv[8];
-      if (qv) unpack_frag(ld_frag(orow + 16 * s + 8 * half), ov);
-      else
-        for (int v = 0; v < 8; ++v) ov[v] = 0.f;
+      unpack_frag(oraw[s], ov);
+#pragma unroll
+      for (int v = 0; v < 8; ++v) ov[v] = qv ? ov[v] : 0.f;
       unpack_frag(df[s], dv);
 #pragma unroll
       for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
     }
     dsum += __shfl_xor(dsum, 32, 64);
   }
-  const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
+  const float lse_raw = a.lse[(long)bh * S + (qv ? q : 0)];
+  const float lse = qv ? lse_raw : 0.f;
   if (qv && half == 0) a.dsum[(long)bh * S + q] = dsum;
 
   f32x16 dq[DH / 32];
@@ -361,8 +368,10 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
     tdo.store(sO, false, S, qt * KT, rtab);
     for (int i = threadIdx.x; i < KT; i += blockDim.x) {
       const int qq = qt * KT + i;
-      sL[i] = qq < S ? a.lse[(long)bh * S + qq] : 0.f;
-      sD[i] = qq < S ? a.dsum[(long)bh * S + qq] : 0.f;
+      const long qi = (long)bh * S + min(qq, S - 1);
+      const float lv = a.lse[qi], dv = a.dsum[qi];
+      sL[i] = qq < S ? lv : 0.f;
+      sD[i] = qq < S ? dv : 0.f;
     }
     // issued after the row statistics: loads complete in order, so waiting
     // for those must not wait for the prefetch
@@ -437,7 +446,8 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   const bf16* dO = static_cast<const bf16*>(a.dout);
 
   // Q, dO, K, V tiles (rows >= S zero; RoPE on Q and K), this lane's O row
-  // and its LSE, every global load issued before the first LDS store.  The
+  // and its LSE, every global load issued before the first LDS store, none
+  // conditional on a lane (rows past S read a valid row, masked afterwards).  The
   // prologue is bound by memory bandwidth (all workgroups load at once), so
   // dO is read once: the row sum D = rowsum(dO * O) takes it from the tile.
   const int q = wave * 32 + l32;
@@ -452,19 +462,23 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   {
     const bf16* orow = static_cast<const bf16*>(a.o) + qrow * a.ld_o + hd * DH;
 #pragma unroll
-    for (int s = 0; s < DH / 16; ++s) orw[s] = qv ? ld_frag(orow + 16 * s + 8 * half) : zero_frag();
+    for (int s = 0; s < DH / 16; ++s) orw[s] = ld_frag(orow + 16 * s + 8 * half);  // qrow clamped
   }
-  const float lse = qv ? a.lse[(long)bh * S + q] : 0.f;
+  const float lse_raw = a.lse[(long)bh * S + (qv ? q : 0)];
   tq.store(sQ, rot_load(a), S, 0, rtab);
   tdo.store(sdO, false, S, 0, rtab);
   tk.store(sK, rot_load(a), S, 0, rtab);
   tv.store(sV, false, S, 0, rtab);
   __syncthreads();
+  // the O row and the LSE were loaded last; masked only here, at their first use
+  const float lse = qv ? lse_raw : 0.f;
   float dsum = 0.f;
 #pragma unroll
   for (int s = 0; s < DH / 16; ++s) {
     float ov[8], dv[8];
     unpack_frag(orw[s], ov);
+#pragma unroll
+    for (int v = 0; v < 8; ++v) ov[v] = qv ? ov[v] : 0.f;
     unpack_frag(ld_frag(sdO + q * (DH + 8) + 16 * s + 8 * half), dv);  // rows >= S are zero
 #pragma unroll
     for (int v = 0; v < 8; ++v) dsum += ov[v] * dv[v];
