@@ -44,6 +44,8 @@ SMALL = {
     # (one 128x192 tile per head and sequence), here on only 8 tiles; at the
     # cut-off c = 1 block 0 keeps no projections, at c = -1 every block does
     "small_bert_s128": Workload("small_bert_s128", "bert", "bf16", 3, 256, 4, 512, 64, 128, 2, 1, "dy", 2011),
+    # d = 512: the row kernels' two-run (512 features per token) instantiation, T = 135
+    "small_bert_d512": Workload("small_bert_d512", "bert", "bf16", 2, 512, 8, 1024, 64, 45, 3, 0, "dy", 2012),
 }
 
 
