@@ -375,12 +375,12 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 }
 
 // ================================================================ bf16 weight gradients
-// C[p][q] += sum_t X[t][p] * Y[t][q]: blockIdx.z = 0 -> dW_up (X = gelu(U), Y = dZ),
+// C[p][q] += sum_t X[t][p] * Y[t][q]: output kind 0 -> dW_up (X = gelu(U), Y = dZ),
 // 1 -> dW_down (X = z, Y = dU).  64x64 output tiles, DW_TC tokens per
 // workgroup.  Token-major tiles go to LDS as they are in memory (16-B chunks);
 // the MFMA operands, which need 8 consecutive tokens per lane, are read with
 // the LDS transpose read.
-// One launch covers up to DW_BATCH adapters: blockIdx.z = 2 * adapter + (0
+// One launch covers up to DW_BATCH adapters: output kind index 2 * adapter + (0
 // up, 1 down).  512-token chunks: with a whole backward's adapters in one
 // launch there are workgroups enough, and each output element takes half the
 // atomic adds of 256-token chunks (1024 would hold every chunk's loads in
@@ -388,25 +388,43 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 constexpr int DW_TC = 512, DW_BATCH = 16;
 struct AdapterDwBatch {
   AdapterDwArgs a[DW_BATCH];
+  int gx, gy;  // 64-column tiles of d and token chunks, per output kind
 };
 __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
   __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [token][p]
   __shared__ __attribute__((aligned(16))) bf16 sY[64 * GP];  // [token][q]
-  const AdapterDwArgs& a = batch.a[blockIdx.z >> 1];
-  const bool up = (blockIdx.z & 1) == 0;
+  // One-dimensional grid of gx * gy * gz workgroups.  The gx column tiles of one (token
+  // chunk, output kind) pair read the same small operand chunk (U or dU, 64 KB); up to
+  // d = 1024 they are placed on one XCD (workgroup i runs on XCD i % 8), consecutively,
+  // so that chunk is fetched into that XCD's L2 once instead of into every XCD's.  Wider
+  // (gx > 16) keeps them spread: one XCD streaming a chunk's whole big operand (64 KB per
+  // tile) through its L2 was slower (d = 4096: 50 -> 58 us).
+  const int gx = batch.gx, gy = batch.gy, npair = gridDim.x / gx;
+  int pair, tile;
+  if (npair % 8 == 0 && gx <= 16) {
+    const int slot = blockIdx.x / 8;
+    pair = (blockIdx.x % 8) * (npair / 8) + slot / gx;
+    tile = slot % gx;
+  } else {
+    pair = blockIdx.x / gx;
+    tile = blockIdx.x % gx;
+  }
+  const int bx = tile, by = pair % gy, bz = pair / gy;
+  const AdapterDwArgs& a = batch.a[bz >> 1];
+  const bool up = (bz & 1) == 0;
   const int d = a.d, T = a.T;
   const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
   const bf16* Y = static_cast<const bf16*>(up ? a.dz : a.du);
   const int ldx = up ? MB : d, ldy = up ? d : MB;
   float* C = up ? a.g_up : a.g_down;
   const int ldc = up ? d : MB;
-  const int p0 = up ? 0 : blockIdx.x * 64, q0 = up ? blockIdx.x * 64 : 0;
+  const int p0 = up ? 0 : bx * 64, q0 = up ? bx * 64 : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, half = lane >> 5;
   const int wp = wave / 2, wq = wave % 2;
   f32x16 acc;
 #pragma unroll
   for (int r = 0; r < 16; ++r) acc[r] = 0.f;
-  const int tbeg = blockIdx.y * DW_TC, tend = min(T, tbeg + DW_TC);
+  const int tbeg = by * DW_TC, tend = min(T, tbeg + DW_TC);
   constexpr int NSUB = DW_TC / 64;
   // every 16-B chunk of the chunk's X and Y rows, loaded before the first use
   bf16x8 xr[NSUB][2], yr[NSUB][2];
@@ -915,8 +933,9 @@ hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, hip
     const int nb = n - k0 < DW_BATCH ? n - k0 : DW_BATCH;
     AdapterDwBatch b{};
     for (int k = 0; k < nb; ++k) b.a[k] = a[k0 + k];
-    const dim3 grid(a[0].d / 64, (a[0].T + DW_TC - 1) / DW_TC, 2 * nb);
-    RG_LAUNCH(adapter_dw_bf16, grid, dim3(256), 0, s, b);
+    b.gx = a[0].d / 64;
+    b.gy = (a[0].T + DW_TC - 1) / DW_TC;
+    RG_LAUNCH(adapter_dw_bf16, dim3((unsigned)(b.gx * b.gy * 2 * nb)), dim3(256), 0, s, b);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
