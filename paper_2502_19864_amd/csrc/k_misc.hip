@@ -82,18 +82,30 @@ __global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm
   __shared__ float red[4];
   const long row = (long)blockIdx.x * d;
   const int nc = d / 8;
+  // every load up front, none conditional on a lane or an operand: a chunk past the row
+  // reads chunk 0, an absent operand reads x1 (gamma) instead, masked afterwards; so no
+  // load waits for the one before it
+  const bf16* x2p = x2 ? x2 : x1;
+  const bf16* gp = gamma ? gamma : x1;
+  const bf16* bp = (norm == Norm::LN && beta) ? beta : gp;
+  bf16x8 r1[NORM_NPT], r2[NORM_NPT], rg[NORM_NPT], rb[NORM_NPT];
+#pragma unroll
+  for (int i = 0; i < NORM_NPT; ++i) {
+    const int c = threadIdx.x + 256 * i, cc = c < nc ? c : 0;
+    r1[i] = ld_frag(x1 + row + 8 * cc);
+    r2[i] = ld_frag(x2p + row + 8 * cc);
+    rg[i] = ld_frag(gp + 8 * cc);
+    rb[i] = ld_frag(bp + 8 * cc);
+  }
   float v[NORM_NPT][8];
 #pragma unroll
   for (int i = 0; i < NORM_NPT; ++i) {
-    const int c = threadIdx.x + 256 * i;
-    if (c >= nc) continue;
-    ld8f(x1 + row + 8 * c, v[i]);
-    if (x2) {
-      float y[8];
-      ld8f(x2 + row + 8 * c, y);
+    float y[8];
+    unpack_frag(r1[i], v[i]);
+    unpack_frag(r2[i], y);
+    if (x2)
 #pragma unroll
       for (int q = 0; q < 8; ++q) v[i][q] += y[q];
-    }
   }
   if (norm == Norm::None || (norm == Norm::RMS && x2)) {
 #pragma unroll
@@ -129,13 +141,13 @@ __global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm
   for (int i = 0; i < NORM_NPT; ++i) {
     const int c = threadIdx.x + 256 * i;
     if (c >= nc) continue;
-    float xh[8], g[8], b[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f}, o[8];
-    ld8f(gamma + 8 * c, g);
-    if (norm == Norm::LN) ld8f(beta + 8 * c, b);
+    float xh[8], g[8], b[8], o[8];
+    unpack_frag(rg[i], g);
+    unpack_frag(rb[i], b);
 #pragma unroll
     for (int q = 0; q < 8; ++q) {
       xh[q] = (v[i][q] - mean) * rs;
-      o[q] = xh[q] * g[q] + b[q];
+      o[q] = xh[q] * g[q] + (norm == Norm::LN ? b[q] : 0.f);
     }
     st8f(dst + row + 8 * c, o);
     if (xhat) st8f(xhat + row + 8 * c, xh);
