@@ -120,13 +120,41 @@ __device__ __forceinline__ void load_row_frags(const bf16* src, int pos, bool va
   for (int s = 0; s < DH / 16; ++s) f[s] = pack_frag(x[s]);
 }
 
+// Causal tiles do unequal work: query tile t of nq takes t + 1 key tiles (the dK/dV
+// pass: key block j takes nq - j query tiles).  At d_h = 128 a workgroup fills its CU,
+// so the CUs take the workgroups in dispatch order as they free up; dispatching the
+// heaviest tiles first (each XCD gets its workgroups in linear-id order, one in eight)
+// keeps the light ones for the end, where the plain order could leave one CU a heavy
+// tile last.  Returns rank 0 for the heaviest tile and the batch-head index; shapes
+// whose workgroups do not split evenly over the XCDs keep xcd_block's order.
+__device__ __forceinline__ void heavy_first(int lin, int nq, int nbh, int& rank, int& bh) {
+  const int n = nq * nbh, P = n / 8;
+  if (n % 8 || P % nq) {
+    const int blk = xcd_block(lin, n);
+    rank = nq - 1 - blk % nq;
+    bh = blk / nq;
+    return;
+  }
+  const int x = lin % 8, o = lin / 8, per = P / nq;  // XCD x, its o-th workgroup
+  rank = o / per;
+  bh = x * per + o % per;
+}
+
 template <int DH, bool CAUSAL, int NW>
 __global__ __launch_bounds__(64 * NW) void attn_fwd_bf16(AttnArgs a) {
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
-  const int qb = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  int qb, bh;
+  if (CAUSAL) {
+    heavy_first(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x, gridDim.y, qb, bh);
+    qb = gridDim.x - 1 - qb;  // query tile t does t + 1 key tiles
+  } else {
+    const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+    qb = blk % gridDim.x;
+    bh = blk / gridDim.x;
+  }
+  const int b = bh / a.H, hd = bh % a.H, S = a.S;
   const int q = qb * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
@@ -231,8 +259,16 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   __shared__ __attribute__((aligned(16))) bf16 sK[KT * (DH + 8)];
   __shared__ __attribute__((aligned(16))) bf16 sV[KT * (DH + 8)];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
-  const int qb = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  int qb, bh;
+  if (CAUSAL) {
+    heavy_first(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x, gridDim.y, qb, bh);
+    qb = gridDim.x - 1 - qb;  // query tile t does t + 1 key tiles
+  } else {
+    const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+    qb = blk % gridDim.x;
+    bh = blk / gridDim.x;
+  }
+  const int b = bh / a.H, hd = bh % a.H, S = a.S;
   const int q = qb * (32 * NW) + wave * 32 + l32;
   const bool qv = q < S;
   const int d = a.H * DH;
@@ -331,8 +367,15 @@ __global__ __launch_bounds__(64 * NW) __attribute__((amdgpu_waves_per_eu(DH <= 6
   __shared__ __attribute__((aligned(16))) bf16 sO[KT * (DH + 8)];
   __shared__ float sL[KT], sD[KT];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, half = lane >> 5, l32 = lane & 31;
-  const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
-  const int kb0 = blk % gridDim.x, bh = blk / gridDim.x, b = bh / a.H, hd = bh % a.H, S = a.S;
+  int kb0, bh;
+  if (CAUSAL) {
+    heavy_first(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x, gridDim.y, kb0, bh);  // block j: nq - j tiles
+  } else {
+    const int blk = xcd_block(blockIdx.x + gridDim.x * blockIdx.y, gridDim.x * gridDim.y);
+    kb0 = blk % gridDim.x;
+    bh = blk / gridDim.x;
+  }
+  const int b = bh / a.H, hd = bh % a.H, S = a.S;
   const int key = kb0 * (32 * NW) + wave * 32 + l32;
   const bool kv = key < S;
   const int d = a.H * DH;
