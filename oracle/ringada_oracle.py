@@ -2,7 +2,8 @@
 
 TEST INFRASTRUCTURE ONLY.  Nothing on the product path may import, call or
 execute this module: it is used by ``tests/``, by ``__graft_entry__.smoke()``
-(as the checker) and by the ``cpu_baseline`` leg of ``bench.py``.  It shares
+(as the reference the GPU result is compared with) and by the ``cpu_baseline``
+leg of ``bench.py``.  It shares
 no code with the HIP library.
 
 What it computes
