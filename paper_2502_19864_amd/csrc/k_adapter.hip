@@ -539,7 +539,9 @@ template <bool BWD>
 __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, const bf16* ui, bf16* uo, int T,
                                                        int d, const bf16* Wb, const bf16* Z, const bf16* R,
                                                        bf16* out) {
+  constexpr int OP = WIDE_UC + 4;  // fp32 pitch of the staged result rows
   __shared__ __attribute__((aligned(16))) bf16 sG[TOK * GP];
+  __shared__ __attribute__((aligned(16))) float sO[TOK * OP];  // G W^T of the chunk, [token][feature]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int t0 = blockIdx.x * TOK, fc = blockIdx.y;
   // Every load is issued before the first use: the split-K partial sums (four chunks per
@@ -556,13 +558,12 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
     for (int q = 0; q < KB; ++q) part[it][q] = P[((long)min(q, nkc - 1) * T + t) * MB + j];
     uiv[it] = BWD ? ui[(long)t * MB + j] : f2bf(0.f);
   }
-  const int token = t0 + l16;
-  const bool tv = token < T;
-  const long row = (long)(tv ? token : 0) * d;
   constexpr int NBK = WIDE_UC / 16 / 4;  // 16-feature blocks per wave
   const int b0 = (fc * WIDE_UC + wave * (WIDE_UC / 4)) / 16;
-  bf16x8 w[NBK][2];
-  uint2 zr[NBK], rr[NBK];
+  // the Z / R rows of the chunk as contiguous 16-B pieces (token c / CPT, features
+  // 8 (c % CPT) ..), the layout the output is stored in, rather than the MFMA layout
+  constexpr int CPT = WIDE_UC / 8, NCK = TOK * CPT / 256;
+  bf16x8 w[NBK][2], zr[NCK], rr[NCK];
   if (Wb) {
 #pragma unroll
     for (int b = 0; b < NBK; ++b) {
@@ -571,11 +572,11 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
     }
     const bf16* Rp = R ? R : Z;
 #pragma unroll
-    for (int b = 0; b < NBK; ++b) {
-      const int f = (b0 + b) * 16 + 4 * grp;
-      zr[b] = *reinterpret_cast<const uint2*>(Z + row + f);
-      const uint2 rv = *reinterpret_cast<const uint2*>(Rp + row + f);
-      rr[b] = R ? rv : make_uint2(0, 0);
+    for (int i = 0; i < NCK; ++i) {
+      const int c = threadIdx.x + 256 * i, t = min(t0 + c / CPT, T - 1);
+      const long off = (long)t * d + fc * WIDE_UC + 8 * (c % CPT);
+      zr[i] = ld_frag(Z + off);
+      rr[i] = ld_frag(Rp + off);
     }
   }
 #pragma unroll
@@ -600,20 +601,27 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
   __syncthreads();
   const bf16x8 g0 = ld_frag(sG + l16 * GP + 8 * grp), g1 = ld_frag(sG + l16 * GP + 32 + 8 * grp);
 #pragma unroll
-  for (int b = 0; b < NBK; ++b) {
+  for (int b = 0; b < NBK; ++b) {  // lane: token l16, features 4 grp .. + 3 of block b
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
     acc = mfma16(w[b][0], g0, acc);
     acc = mfma16(w[b][1], g1, acc);
-    if (!tv) continue;
-    float o[4];
+    *reinterpret_cast<float4*>(sO + l16 * OP + wave * (WIDE_UC / 4) + b * 16 + 4 * grp) =
+        make_float4(acc[0], acc[1], acc[2], acc[3]);
+  }
+  __syncthreads();
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const uint32_t zw = q < 2 ? zr[b].x : zr[b].y, rw = q < 2 ? rr[b].x : rr[b].y;
-      const float zf = __uint_as_float((q & 1) ? (zw & 0xffff0000u) : (zw << 16));
-      const float rf = __uint_as_float((q & 1) ? (rw & 0xffff0000u) : (rw << 16));
-      o[q] = acc[q] + zf + rf;
-    }
-    St<bf16>::st4(out, row + (b0 + b) * 16 + 4 * grp, o);
+  for (int i = 0; i < NCK; ++i) {
+    const int c = threadIdx.x + 256 * i, tok = c / CPT, f8 = 8 * (c % CPT);
+    if (t0 + tok >= T) continue;
+    float o[8], zf[8], rf[8];
+    const float4 lo = *reinterpret_cast<const float4*>(sO + tok * OP + f8);
+    const float4 hi = *reinterpret_cast<const float4*>(sO + tok * OP + f8 + 4);
+    unpack_frag(zr[i], zf);
+    unpack_frag(rr[i], rf);
+    const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
+#pragma unroll
+    for (int q = 0; q < 8; ++q) o[q] = v[q] + zf[q] + (R ? rf[q] : 0.f);
+    *reinterpret_cast<bf16x8*>(out + (long)(t0 + tok) * d + fc * WIDE_UC + f8) = pack_frag(o);
   }
 }
 
