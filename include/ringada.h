@@ -31,9 +31,11 @@
  *   - Errors are returned as a status; the message of the last failing call on
  *     the calling thread is available from ringada_last_error().  The library
  *     never aborts and never prints.
- *   - Per-step calls (forward, backward, adapter step, losses) allocate no
- *     device memory.  ringada_stage_bind_block allocates the library's own
- *     copies of the weights (see there); ringada_stage_destroy frees them.
+ *   - The library allocates no device memory, in any call.  Every device
+ *     buffer is the caller's: frozen weights, adapter masters and gradients,
+ *     the activation stash and scratch (ringada_stage_plan), and the regions
+ *     that hold what the library derives from the weights
+ *     (ringada_stage_plan_weights).
  */
 #ifndef RINGADA_H
 #define RINGADA_H
@@ -152,28 +154,56 @@ int32_t ringada_local_cutoff(int32_t n_tm, int32_t depth, int32_t first_block,
 
 /* ---------------------------------------------------------------- lifetime */
 
-/* Validates desc and creates a handle on the current HIP device.  No device
- * memory is allocated here. */
-ringada_status ringada_stage_create(const ringada_stage_desc* desc,
-                                    ringada_stage** out);
+/* Host only.  Bytes of the caller memory that holds what the library
+ * derives from the weights:
+ *   block_bytes: per block, passed to ringada_stage_bind_block: a transposed
+ *     copy of each frozen projection matrix ([out, in], so that both operands
+ *     of every forward product are contiguous along the contraction; post-LN
+ *     bf16 stages with d_head 64 keep the QKV rows, and a copy of the QKV
+ *     bias, in per-head order [Q_h K_h V_h]; pre-RMS stages interleave the
+ *     gate and up rows in 32-row groups) and the adapters' working copies in
+ *     the stage dtype (W_down, W_up and their transposes, fragment-packed in
+ *     bf16 stages), 4 d m elements per adapter;
+ *   stage_bytes: per stage, passed to ringada_stage_create: the rotary
+ *     (cos, sin) table of the pre-RMS arch, max_seq x d_head/2 float pairs
+ *     (0 for the post-LN arch).
+ * Either output pointer may be NULL. */
+ringada_status ringada_stage_plan_weights(const ringada_stage_desc* desc,
+                                          size_t* block_bytes, size_t* stage_bytes);
+
+/* Validates desc and creates a handle on the current HIP device.  stage_mem:
+ * device memory of at least the stage_bytes of ringada_stage_plan_weights
+ * (may be NULL when that is 0), 256-byte aligned, owned by the caller and
+ * borrowed until ringada_stage_destroy; the first ringada_stage_bind_block
+ * fills it.  Allocates nothing; RINGADA_E_WORKSPACE if stage_mem is too
+ * small. */
+ringada_status ringada_stage_create(const ringada_stage_desc* desc, void* stage_mem,
+                                    size_t stage_mem_bytes, ringada_stage** out);
 
 /* Binds block `block` (0-indexed, local).  Frozen weights and the adapters
  * are borrowed; under RINGADA_PLACEMENT_FFN attn_adapter must be NULL (the
- * block has none), otherwise both are required.  The library allocates, on the current device, a transposed copy
- * of each frozen projection matrix (the forward multiplies by it; the frozen
- * weights never change, so the copy stays valid) and working copies of the
- * adapters in the stage dtype, fills them on `stream` and synchronises the
- * stream before returning.  Binding a block again replaces its bindings. */
+ * block has none), otherwise both are required.  block_mem: device memory of
+ * at least the block_bytes of ringada_stage_plan_weights, 256-byte aligned,
+ * owned by the caller, borrowed until ringada_stage_destroy; the library
+ * writes into it the transposed projections (the frozen weights never
+ * change, so the copies stay valid) and the adapters' working copies, which
+ * every ringada_adapter_step refreshes.  Fills it on `stream` and
+ * synchronises the stream before returning.  Allocates nothing;
+ * RINGADA_E_WORKSPACE if block_mem is too small.  Binding a block again
+ * replaces its bindings. */
 ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t block,
                                         const ringada_block_weights* frozen,
                                         const ringada_adapter* attn_adapter,
                                         const ringada_adapter* ffn_adapter,
+                                        void* block_mem, size_t block_mem_bytes,
                                         void* stream);
 
 /* Re-derives the adapter working copies from the fp32 masters (call after
  * writing the masters directly, e.g. when loading a checkpoint). */
 ringada_status ringada_stage_sync_adapters(ringada_stage* st, void* stream);
 
+/* Releases the handle (host memory only; every device buffer stays the
+ * caller's). */
 void ringada_stage_destroy(ringada_stage* st);
 
 /* ---------------------------------------------------------------- hot path */
@@ -183,9 +213,10 @@ void ringada_stage_destroy(ringada_stage* st);
  * for the backward (see ringada_stage_plan); stash/scratch are caller buffers
  * of at least the planned sizes and must stay untouched until the matching
  * backward has been enqueued.
- * State machine: with c < n_blocks the handle becomes "pending" and another
- * forward returns RINGADA_E_STATE until ringada_stage_backward has been
- * called; with c >= n_blocks (frozen stage) forwards may follow each other. */
+ * State machine: with c < n_blocks the handle becomes "pending" and every
+ * further forward (a frozen one included) returns RINGADA_E_STATE until
+ * ringada_stage_backward has been called; with c >= n_blocks (frozen stage)
+ * nothing is left pending, so such forwards may follow each other. */
 ringada_status ringada_stage_forward(ringada_stage* st, void* stream,
                                      const void* x, void* y, int32_t batch,
                                      int32_t seq, int32_t lowest_unfrozen,
@@ -210,7 +241,9 @@ ringada_status ringada_stage_backward(ringada_stage* st, void* stream,
 
 /* Update of the unfrozen adapters (blocks l >= max(c, 0)) from their
  * accumulated gradients (Sec. III-B: clients with unfrozen adapters update
- * them), then zero the gradients and refresh the working copies. */
+ * them), then zero the gradients and refresh the working copies.  Returns
+ * RINGADA_E_STATE while a forward is pending its backward (the backward
+ * must see the weights the forward used). */
 ringada_status ringada_adapter_step(ringada_stage* st, void* stream,
                                     int32_t lowest_unfrozen,
                                     const ringada_optim* opt);

@@ -53,9 +53,10 @@ SIGNATURES = [
     ("ringada_stage_plan", c_int32, [POINTER(StageDesc), c_int32, c_int32, c_int32,
                                      POINTER(c_size_t), POINTER(c_size_t)]),
     ("ringada_local_cutoff", c_int32, [c_int32, c_int32, c_int32, c_int32]),
-    ("ringada_stage_create", c_int32, [POINTER(StageDesc), POINTER(c_void_p)]),
+    ("ringada_stage_plan_weights", c_int32, [POINTER(StageDesc), POINTER(c_size_t), POINTER(c_size_t)]),
+    ("ringada_stage_create", c_int32, [POINTER(StageDesc), c_void_p, c_size_t, POINTER(c_void_p)]),
     ("ringada_stage_bind_block", c_int32, [c_void_p, c_int32, POINTER(BlockWeights), POINTER(Adapter),
-                                           POINTER(Adapter), c_void_p]),
+                                           POINTER(Adapter), c_void_p, c_size_t, c_void_p]),
     ("ringada_stage_sync_adapters", c_int32, [c_void_p, c_void_p]),
     ("ringada_stage_destroy", None, [c_void_p]),
     ("ringada_stage_forward", c_int32, [c_void_p, c_void_p, c_void_p, c_void_p, c_int32, c_int32, c_int32,
@@ -115,17 +116,23 @@ def ringada_local_cutoff(n_tm, depth, first_block, n_local):
     return lib().ringada_local_cutoff(n_tm, depth, first_block, n_local)
 
 
-def ringada_stage_create(desc):
+def ringada_stage_plan_weights(desc):
+    blk, stg = c_size_t(0), c_size_t(0)
+    _check(lib().ringada_stage_plan_weights(byref(desc), byref(blk), byref(stg)))
+    return blk.value, stg.value
+
+
+def ringada_stage_create(desc, stage_mem, stage_mem_bytes):
     h = c_void_p()
-    _check(lib().ringada_stage_create(byref(desc), byref(h)))
+    _check(lib().ringada_stage_create(byref(desc), _p(stage_mem), stage_mem_bytes, byref(h)))
     return h
 
 
-def ringada_stage_bind_block(stage, block, frozen, attn_adapter, ffn_adapter, stream):
+def ringada_stage_bind_block(stage, block, frozen, attn_adapter, ffn_adapter, block_mem, block_mem_bytes, stream):
     """attn_adapter is None for a stage with the single (FFN) placement."""
     _check(lib().ringada_stage_bind_block(stage, block, byref(frozen),
                                           None if attn_adapter is None else byref(attn_adapter),
-                                          byref(ffn_adapter), stream))
+                                          byref(ffn_adapter), _p(block_mem), block_mem_bytes, stream))
 
 
 def ringada_stage_sync_adapters(stage, stream):

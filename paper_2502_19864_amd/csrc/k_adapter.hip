@@ -382,13 +382,18 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 // the LDS transpose read.
 // One launch covers up to DW_BATCH adapters: output kind index 2 * adapter + (0
 // up, 1 down).  512-token chunks: with a whole backward's adapters in one
-// launch there are workgroups enough, and each output element takes half the
-// atomic adds of 256-token chunks (1024 would hold every chunk's loads in
-// 256 registers).
+// launch there are workgroups enough (1024 would hold every chunk's loads in
+// 256 registers).  Each workgroup stores its chunk's 64x64 partial sum with
+// plain stores into part ([kind][chunk][m d], the element order of the
+// gradient itself); adapter_dw_reduce then adds the chunks, in chunk order,
+// into the gradient.  So the result does not depend on the order in which
+// workgroups finish: the same inputs give the same bits, whatever else the
+// launch carries.
 constexpr int DW_TC = 512, DW_BATCH = 16;
 struct AdapterDwBatch {
   AdapterDwArgs a[DW_BATCH];
   int gx, gy;  // 64-column tiles of d and token chunks, per output kind
+  float* part;
 };
 __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
   __shared__ __attribute__((aligned(16))) bf16 sX[64 * GP];  // [token][p]
@@ -416,7 +421,6 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
   const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
   const bf16* Y = static_cast<const bf16*>(up ? a.dz : a.du);
   const int ldx = up ? MB : d, ldy = up ? d : MB;
-  float* C = up ? a.g_up : a.g_down;
   const int ldc = up ? d : MB;
   const int p0 = up ? 0 : bx * 64, q0 = up ? bx * 64 : 0;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, half = lane >> 5;
@@ -461,11 +465,33 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
                    acc);
   }
   // D[i = p][j = q]: lane holds q = wq*32 + l32, p = wp*32 + 8*(r/4) + 4*half + r%4
+  float* P = batch.part + ((long)bz * gy + by) * ((long)MB * d);
 #pragma unroll
   for (int r = 0; r < 16; ++r) {
     const int p = p0 + wp * 32 + 8 * (r >> 2) + 4 * half + (r & 3), q = q0 + wq * 32 + l32;
-    unsafeAtomicAdd(C + (long)p * ldc + q, acc[r]);
+    P[(long)p * ldc + q] = acc[r];
   }
+}
+
+// C += sum over the chunks c = 0, 1, .. of part[kind][c] (in that order), four
+// consecutive elements per thread, for every output kind of the batch
+__global__ __launch_bounds__(256) void adapter_dw_reduce(AdapterDwBatch batch, int nkind) {
+  const long md = (long)MB * batch.a[0].d, per = md / 4;
+  const long i = (long)blockIdx.x * 256 + threadIdx.x;
+  if (i >= nkind * per) return;
+  const int bz = (int)(i / per);
+  const long e = (i % per) * 4;
+  const AdapterDwArgs& a = batch.a[bz >> 1];
+  float* C = ((bz & 1) == 0 ? a.g_up : a.g_down) + e;
+  const float* src = batch.part + (long)bz * batch.gy * md + e;
+  float4 s = *reinterpret_cast<const float4*>(src);
+  for (int c = 1; c < batch.gy; ++c) {
+    const float4 v = *reinterpret_cast<const float4*>(src + c * md);
+    s.x += v.x; s.y += v.y; s.z += v.z; s.w += v.w;
+  }
+  float4 g = *reinterpret_cast<const float4*>(C);
+  g.x += s.x; g.y += s.y; g.z += s.z; g.w += s.w;
+  *reinterpret_cast<float4*>(C) = g;
 }
 
 // ================================================================ bf16, d > 1024
@@ -913,37 +939,46 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
   return hipGetLastError();
 }
 
-hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s) {
-  if (a.T < 0 || !a.u || !a.dz || !a.z || !a.du || !a.g_up || !a.g_down) return hipErrorInvalidValue;
-  if (a.T == 0) return hipSuccess;
-  if (dtype == DT_BF16) return launch_adapter_dw_batch(dtype, &a, 1, s);
-  const long n = 2L * a.m * a.d;
-  RG_LAUNCH(adapter_dw_f32, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
-  return hipGetLastError();
+long adapter_dw_part_bytes(int dtype, int T, int d, int m, int n_adapters) {
+  if (dtype != DT_BF16 || T <= 0 || n_adapters <= 0) return 0;
+  const long nb = n_adapters < DW_BATCH ? n_adapters : DW_BATCH;
+  return nb * 2 * ((T + DW_TC - 1) / DW_TC) * (long)d * m * 4;
 }
 
-hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, hipStream_t s) {
+hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, float* part, long part_bytes,
+                                   hipStream_t s) {
   if (n < 0 || (n > 0 && !a)) return hipErrorInvalidValue;
+  for (int k = 0; k < n; ++k) {
+    const AdapterDwArgs& x = a[k];
+    if (x.T < 0 || !x.u || !x.dz || !x.z || !x.du || !x.g_up || !x.g_down) return hipErrorInvalidValue;
+  }
+  if (n == 0 || a[0].T == 0) return hipSuccess;
   if (dtype != DT_BF16) {
     for (int k = 0; k < n; ++k) {
-      const hipError_t e = launch_adapter_dw(dtype, a[k], s);
+      const long ne = 2L * a[k].m * a[k].d;
+      RG_LAUNCH(adapter_dw_f32, dim3((unsigned)((ne + 255) / 256)), dim3(256), 0, s, a[k]);
+      const hipError_t e = hipGetLastError();
       if (e != hipSuccess) return e;
     }
     return hipSuccess;
   }
   for (int k = 0; k < n; ++k) {
     const AdapterDwArgs& x = a[k];
-    if (x.T < 0 || !x.u || !x.dz || !x.z || !x.du || !x.g_up || !x.g_down) return hipErrorInvalidValue;
     if (x.T != a[0].T || x.d != a[0].d || x.m != a[0].m || x.m != MB || x.d % 64) return hipErrorInvalidValue;
+    if (!al16(x.g_up) || !al16(x.g_down)) return hipErrorInvalidValue;
   }
-  if (n == 0 || a[0].T == 0) return hipSuccess;
+  if (!part || !al16(part) || part_bytes < adapter_dw_part_bytes(dtype, a[0].T, a[0].d, a[0].m, n))
+    return hipErrorInvalidValue;
   for (int k0 = 0; k0 < n; k0 += DW_BATCH) {
     const int nb = n - k0 < DW_BATCH ? n - k0 : DW_BATCH;
     AdapterDwBatch b{};
     for (int k = 0; k < nb; ++k) b.a[k] = a[k0 + k];
     b.gx = a[0].d / 64;
     b.gy = (a[0].T + DW_TC - 1) / DW_TC;
+    b.part = part;
     RG_LAUNCH(adapter_dw_bf16, dim3((unsigned)(b.gx * b.gy * 2 * nb)), dim3(256), 0, s, b);
+    const long per = (long)MB * a[0].d / 4;
+    RG_LAUNCH(adapter_dw_reduce, dim3((unsigned)((2 * nb * per + 255) / 256)), dim3(256), 0, s, b, 2 * nb);
     const hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }

@@ -1,8 +1,10 @@
 // Attention core of the frozen blocks: softmax(Q K^T / sqrt(d_head) [+causal]) V
 // per (batch, head), and its backward (dQ, dK, dV; frozen projections around it
-// are plain GEMMs).  Rotary embedding (rotate-half pairs (i, i + d_head/2)) is
-// applied to Q and K as they are loaded, so the stash keeps the pre-rotation
-// projections and the backward rotates the gradients back.
+// are plain GEMMs).  Rotary embedding (rotate-half pairs (i, i + d_head/2)):
+// in bf16 stages the QKV projection's epilogue has already rotated Q and K, so
+// the stash holds the rotated projections and the kernels load them as they
+// are; the fp32 path rotates Q and K as they are loaded.  Either way the
+// backward rotates dQ and dK back before storing them.
 //
 // bf16 kernels use MFMA 32x32x16 with K/V (or Q/dO) tiles staged in LDS.
 // Each wave owns 32 queries (forward, dQ pass) or 32 keys (dK/dV pass), so the

@@ -527,7 +527,10 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
     constexpr int DHA = 64, TPA = DHA + 8, TILE = BM * TPA;
     static_assert(3 * TILE * 2 + BIASB <= NS * STAGE, "Q, K, V tiles and the bias fit the stage buffers");
     bf16* sT = reinterpret_cast<bf16*>(smem);
-    barrier();  // the bias is in LDS
+    // the bias stores of the first BN/8 threads must have completed before any
+    // other wave reads them: s_barrier alone does not wait for LDS writes
+    wait_vm_lgkm<0>();
+    barrier();
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll

@@ -257,8 +257,17 @@ hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* d
 }
 
 // ---------------------------------------------------------------- layouts
+// out[c', r] = in[r, c] with c' = c, or, with perm_dh > 0, the per-head order
+// of a [Q | K | V] column block: column p * (cols / 3) + h * perm_dh + i goes
+// to row (3 h + p) * perm_dh + i.
+__device__ __forceinline__ int perm_col(int c, int cols, int perm_dh) {
+  if (perm_dh <= 0) return c;
+  const int blk = cols / 3, p = c / blk, rem = c % blk, h = rem / perm_dh, i = rem % perm_dh;
+  return (3 * h + p) * perm_dh + i;
+}
+
 template <typename Ti, typename To>
-__global__ __launch_bounds__(256) void transpose_k(const Ti* in, int rows, int cols, To* out) {
+__global__ __launch_bounds__(256) void transpose_k(const Ti* in, int rows, int cols, To* out, int perm_dh) {
   __shared__ float tile[32][33];
   const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32, tx = threadIdx.x % 32, ty = threadIdx.x / 32;
   for (int i = ty; i < 32; i += 8) {
@@ -268,20 +277,21 @@ __global__ __launch_bounds__(256) void transpose_k(const Ti* in, int rows, int c
   __syncthreads();
   for (int i = ty; i < 32; i += 8) {
     const int c = c0 + i, r = r0 + tx;
-    if (c < cols && r < rows) St<To>::st(out, (long)c * rows + r, tile[tx][i]);
+    if (c < cols && r < rows) St<To>::st(out, (long)perm_col(c, cols, perm_dh) * rows + r, tile[tx][i]);
   }
 }
 
 hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int rows, int cols, void* out,
-                            hipStream_t s) {
+                            hipStream_t s, int perm_dh) {
   if (!in || !out || rows <= 0 || cols <= 0) return hipErrorInvalidValue;
+  if (perm_dh > 0 && (cols % 3 || (cols / 3) % perm_dh)) return hipErrorInvalidValue;
   const dim3 grid((cols + 31) / 32, (rows + 31) / 32), block(256);
   if (in_dtype == DT_F32 && out_dtype == DT_F32)
-    RG_LAUNCH((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out);
+    RG_LAUNCH((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out, perm_dh);
   else if (in_dtype == DT_F32 && out_dtype == DT_BF16)
-    RG_LAUNCH((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out);
+    RG_LAUNCH((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out, perm_dh);
   else if (in_dtype == DT_BF16 && out_dtype == DT_BF16)
-    RG_LAUNCH((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out);
+    RG_LAUNCH((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out, perm_dh);
   else
     return hipErrorInvalidValue;
   return hipGetLastError();
@@ -308,10 +318,11 @@ hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* o
 
 // ---------------------------------------------------------------- adapter update
 // Element idx < d*m is W_down[i][j] (i = idx / m, j = idx % m); the rest is
-// W_up[j][i].  Writes the working copies W, W^T in the stage dtype.
+// W_up[j][i].  Writes the working copies W, W^T in the stage dtype.  The
+// slots of one launch travel by value (blockIdx.y selects one).
 template <typename T, bool UPDATE>
-__global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots, int d, int m, float lr) {
-  const AdapterSlot sl = slots[blockIdx.y];
+__global__ __launch_bounds__(256) void adapter_update_k(AdapterSlotBatch batch, int d, int m, float lr) {
+  const AdapterSlot& sl = batch.s[blockIdx.y];
   if (!sl.w_down) return;  // a block without this adapter (single placement)
   const long n = (long)d * m;
   for (long idx = (long)blockIdx.x * blockDim.x + threadIdx.x; idx < 2 * n; idx += (long)gridDim.x * blockDim.x) {
@@ -353,13 +364,20 @@ __global__ __launch_bounds__(256) void adapter_update_k(const AdapterSlot* slots
 template <bool UPDATE>
 static hipError_t adapter_update(int dtype, const AdapterSlot* slots, int n_slots, int d, int m, float lr,
                                  hipStream_t s) {
-  if (!slots || n_slots < 0 || d <= 0 || m <= 0) return hipErrorInvalidValue;
-  if (n_slots == 0) return hipSuccess;
+  if ((!slots && n_slots) || n_slots < 0 || d <= 0 || m <= 0) return hipErrorInvalidValue;
   const long n = 2L * d * m;
-  const dim3 grid((unsigned)((n + 255) / 256 < 256 ? (n + 255) / 256 : 256), n_slots), block(256);
-  if (dtype == DT_BF16) RG_LAUNCH((adapter_update_k<bf16, UPDATE>), grid, block, 0, s, slots, d, m, lr);
-  else RG_LAUNCH((adapter_update_k<float, UPDATE>), grid, block, 0, s, slots, d, m, lr);
-  return hipGetLastError();
+  const unsigned gx = (unsigned)((n + 255) / 256 < 256 ? (n + 255) / 256 : 256);
+  for (int i0 = 0; i0 < n_slots; i0 += ADAPTER_SLOT_BATCH) {
+    AdapterSlotBatch b{};
+    const int k = n_slots - i0 < ADAPTER_SLOT_BATCH ? n_slots - i0 : ADAPTER_SLOT_BATCH;
+    for (int i = 0; i < k; ++i) b.s[i] = slots[i0 + i];
+    const dim3 grid(gx, k), block(256);
+    if (dtype == DT_BF16) RG_LAUNCH((adapter_update_k<bf16, UPDATE>), grid, block, 0, s, b, d, m, lr);
+    else RG_LAUNCH((adapter_update_k<float, UPDATE>), grid, block, 0, s, b, d, m, lr);
+    const hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  return hipSuccess;
 }
 
 hipError_t launch_adapter_sgd(int dtype, const AdapterSlot* slots, int n_slots, int d, int m, float lr,
@@ -396,12 +414,7 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
 // Initiator's classification head on the [CLS] (position 0) token of each
 // sample: logits = y[b, 0, :] W_h + b_h, mean cross-entropy over the batch,
 // dy[b, 0, :] = dlogits W_h^T and zero at every other position, and the head
-// gradients accumulated into gwh / gbh.  Workgroup 0 does the head: W_h and,
-// per chunk of `chunk` samples, their [CLS] rows are copied to LDS with
-// 16-B loads (all in flight together); then (1) one wave per sample forms the
-// logits and dlogits, (2) one thread per feature i accumulates gwh[i, :] over
-// the chunk and writes dy[b, 0, i].  It alone owns gwh / gbh / loss, so no
-// atomics are needed.  The other workgroups zero dy at positions 1..S-1.
+// gradients and the loss accumulated into gwh / gbh / loss.
 constexpr int HEAD_C = 16;   // maximum number of classes
 constexpr int HEAD_SPW = 4;  // samples per workgroup (one wave each)
 // Workgroups 0 .. ceil(B / HEAD_SPW) - 1: one wave per sample for the logits,

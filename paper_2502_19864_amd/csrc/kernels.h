@@ -157,9 +157,15 @@ struct AdapterDwArgs {
   float* g_up;     // [m, d]
   float* g_down;   // [d, m]
 };
-hipError_t launch_adapter_dw(int dtype, const AdapterDwArgs& a, hipStream_t s);
-// n adapters' weight gradients (same T, d, m) in as few launches as possible
-hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, hipStream_t s);
+// bytes of the fp32 per-chunk partial sums launch_adapter_dw_batch needs for
+// n adapters (0 for fp32 stages)
+long adapter_dw_part_bytes(int dtype, int T, int d, int m, int n_adapters);
+// n adapters' weight gradients (same T, d, m), added into g_up / g_down in as
+// few launches as possible; bf16: per-chunk partial sums in `part` (16-B
+// aligned, adapter_dw_part_bytes), then a fixed-order reduction, so the result
+// is bitwise reproducible; g_up / g_down 16-B aligned
+hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, float* part, long part_bytes,
+                                   hipStream_t s);
 
 // ---------------------------------------------------------------- row kernels
 // out = RMSNorm(x) * g, xhat/rstd stashes optional
@@ -181,22 +187,29 @@ hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* d
                           hipStream_t s);
 
 // ---------------------------------------------------------------- parameters
-// out[c, r] = in[r, c] (rows x cols), converting float -> stage dtype
+// out[c, r] = in[r, c] (rows x cols), converting float -> stage dtype; with
+// perm_dh > 0 the columns of a [Q | K | V] block (cols = 3 d) come out in
+// per-head order: column p d + h perm_dh + i becomes row (3 h + p) perm_dh + i
 hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int rows, int cols,
-                            void* out, hipStream_t s);
+                            void* out, hipStream_t s, int perm_dh = 0);
 // pack W_gu [d, 2F] into B rows for the SwiGlu epilogue: row p of the result
 // (2F x d) is gate column (p/64)*32 + p%32 if p%64 < 32, else the matching up column
 hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s);
 
-struct AdapterSlot {  // device-side table entry for the update kernel
+struct AdapterSlot {  // one adapter for the update kernel
   float* w_down; float* w_up; float* g_down; float* g_up;
   void* wdn; void* wdn_t; void* wup; void* wup_t;  // working copies
 };
-// SGD on n_slots adapters, zero grads, refresh working copies
-hipError_t launch_adapter_sgd(int dtype, const AdapterSlot* slots_dev, int n_slots, int d, int m,
+constexpr int ADAPTER_SLOT_BATCH = 16;  // slots passed by value per launch
+struct AdapterSlotBatch {
+  AdapterSlot s[ADAPTER_SLOT_BATCH];
+};
+// SGD on n_slots adapters (a host array; launched in batches of
+// ADAPTER_SLOT_BATCH), zero grads, refresh working copies
+hipError_t launch_adapter_sgd(int dtype, const AdapterSlot* slots, int n_slots, int d, int m,
                               float lr, hipStream_t s);
 // refresh working copies only
-hipError_t launch_adapter_sync(int dtype, const AdapterSlot* slots_dev, int n_slots, int d, int m,
+hipError_t launch_adapter_sync(int dtype, const AdapterSlot* slots, int n_slots, int d, int m,
                                hipStream_t s);
 
 // ---------------------------------------------------------------- losses

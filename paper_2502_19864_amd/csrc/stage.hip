@@ -71,6 +71,10 @@ struct Layout {
   // weight-gradient launch at the end of the backward
   std::vector<size_t> gdz, gdu;
   size_t adp;  // both passes
+  // per-chunk partial sums of the weight-gradient launch at the end of the
+  // backward; they take the place of the backward's temporaries, all dead by
+  // then, when those span enough bytes
+  size_t dwp, dwp_bytes;
 };
 
 static size_t al256(size_t n) { return (n + 255) & ~(size_t)255; }
@@ -156,15 +160,20 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   L.dqkv = take(T3d);
   L.dsum = take(lse);
   L.dn1 = llama ? take(Td) : NONE;
+  const size_t temporaries = cur;
   L.gdz.assign(2 * D.n_blocks, NONE);
   L.gdu.assign(2 * D.n_blocks, NONE);
+  int n_dw = 0;
   for (int l = 0; l < D.n_blocks; ++l) {
     if (block_kind(l, c, D.n_blocks) == K_NONE) continue;
     for (int a = single ? 1 : 0; a < 2; ++a) {
       L.gdz[2 * l + a] = take(Td);
       L.gdu[2 * l + a] = take(Tm);
+      ++n_dw;
     }
   }
+  L.dwp_bytes = al256((size_t)adapter_dw_part_bytes(D.dtype, (int)T, (int)d, (int)m, n_dw));
+  L.dwp = L.dwp_bytes == 0 ? NONE : (L.dwp_bytes <= temporaries ? 0 : take(L.dwp_bytes));
   // split-K partials of the wide (d > 1024) adapter kernels, used inside one
   // adapter call in either pass: after both lists
   const long part = adapter_part_elems(D.dtype, (int)T, (int)d, (int)m);
@@ -236,6 +245,49 @@ extern "C" int32_t ringada_local_cutoff(int32_t n_tm, int32_t depth, int32_t fir
   return g - first_block;
 }
 
+// ================================================================ weight memory
+// The library's own copies of what it derives from the frozen weights and
+// the adapters live in caller memory: one region per block, one per stage.
+// Offsets are 256-B aligned relative to the region's base.
+struct WeightLayout {
+  size_t qkv, bqkv, o, in, out;  // transposed projections (+ the per-head-order bias)
+  size_t wk[2][4];               // adapter working copies: W_down, W_down^T, W_up, W_up^T
+  size_t block_bytes;
+  size_t rope, stage_bytes;      // rotary (cos, sin) table
+};
+
+static bool per_head_qkv(const ringada_stage_desc& D) {
+  return D.dtype == RINGADA_BF16 && D.arch == RINGADA_ARCH_POSTLN_GELU && D.d_model == 64 * D.n_heads;
+}
+
+static void plan_weights(const ringada_stage_desc& D, WeightLayout& W) {
+  const size_t es = D.dtype == RINGADA_BF16 ? 2 : 4;
+  const size_t d = D.d_model, F = D.d_ffn, m = D.d_adapter;
+  const bool post = D.arch == RINGADA_ARCH_POSTLN_GELU, single = D.placement == RINGADA_PLACEMENT_FFN;
+  size_t cur = 0;
+  auto take = [&](size_t n) { size_t o = cur; cur += al256(n); return o; };
+  W.qkv = take(3 * d * d * es);
+  W.bqkv = per_head_qkv(D) ? take(3 * d * es) : NONE;
+  W.o = take(d * d * es);
+  W.in = take((post ? 1 : 2) * F * d * es);
+  W.out = take(d * F * es);
+  for (int a = 0; a < 2; ++a)
+    for (int k = 0; k < 4; ++k) W.wk[a][k] = (single && a == 0) ? NONE : take(d * m * es);
+  W.block_bytes = cur;
+  W.rope = post ? NONE : 0;
+  W.stage_bytes = post ? 0 : al256((size_t)D.max_seq * (d / D.n_heads / 2) * sizeof(float2));
+}
+
+extern "C" ringada_status ringada_stage_plan_weights(const ringada_stage_desc* desc, size_t* block_bytes,
+                                                     size_t* stage_bytes) {
+  RG_TRY(check_desc(desc));
+  WeightLayout W;
+  plan_weights(*desc, W);
+  if (block_bytes) *block_bytes = W.block_bytes;
+  if (stage_bytes) *stage_bytes = W.stage_bytes;
+  return RINGADA_OK;
+}
+
 // ================================================================ handle
 struct BlockBind {
   bool bound = false;
@@ -258,10 +310,11 @@ struct ProfRec {
 struct ringada_stage {
   ringada_stage_desc D{};
   int device = 0;
+  WeightLayout WL{};
   std::vector<BlockBind> blocks;
-  std::vector<void*> allocs;
-  AdapterSlot* slots_dev = nullptr;
-  float2* rope_tab = nullptr;  // rotary (cos, sin) [max_seq][d_head/2], built at the first bind
+  char* stage_mem = nullptr;   // caller's per-stage region
+  float2* rope_tab = nullptr;  // rotary (cos, sin) [max_seq][d_head/2] in stage_mem, built at the first bind
+  bool rope_built = false;
   // bf16 post-LN stages with d_head 64 keep Q, K, V in per-head column order
   // [Q_h K_h V_h] (projection weight rows and bias permuted at bind): a
   // 128x192 tile of the QKV projection is then one head of one sequence, and
@@ -270,8 +323,7 @@ struct ringada_stage {
   // weight-gradient work of the adapters back-propagated so far in this
   // backward, launched together when it ends
   std::vector<AdapterDwArgs> dw_pending;
-  void* qkv_tmp = nullptr;     // [3d, d] transposed projection before its rows are permuted
-  std::vector<AdapterSlot> slots;
+  std::vector<AdapterSlot> slots;  // [2 l + a], passed to the update kernel by value
   // state machine
   bool pending = false;
   Layout L;
@@ -284,22 +336,26 @@ struct ringada_stage {
   size_t evused = 0;
 };
 
-static ringada_status dalloc(ringada_stage* st, size_t bytes, void** out) {
-  RG_HIP(hipMalloc(out, bytes));
-  st->allocs.push_back(*out);
-  return RINGADA_OK;
-}
-
-extern "C" ringada_status ringada_stage_create(const ringada_stage_desc* desc, ringada_stage** out) {
+extern "C" ringada_status ringada_stage_create(const ringada_stage_desc* desc, void* stage_mem,
+                                               size_t stage_mem_bytes, ringada_stage** out) {
   if (!out) return fail(RINGADA_E_INVALID, "out is NULL");
   *out = nullptr;
   RG_TRY(check_desc(desc));
+  WeightLayout W;
+  plan_weights(*desc, W);
+  if (stage_mem_bytes < W.stage_bytes || (W.stage_bytes && !stage_mem))
+    return fail(RINGADA_E_WORKSPACE, "stage memory of %zu bytes, the stage needs %zu", stage_mem_bytes,
+                W.stage_bytes);
+  if (reinterpret_cast<uintptr_t>(stage_mem) & 255u)
+    return fail(RINGADA_E_INVALID, "stage memory must be 256-byte aligned");
   ringada_stage* st = new ringada_stage();
   st->D = *desc;
-  st->qkv_per_head = desc->dtype == RINGADA_BF16 && desc->arch == RINGADA_ARCH_POSTLN_GELU &&
-                     desc->d_model == 64 * desc->n_heads;
+  st->WL = W;
+  st->qkv_per_head = per_head_qkv(*desc);
   st->blocks.resize(desc->n_blocks);
   st->slots.assign(2 * desc->n_blocks, AdapterSlot{});
+  st->stage_mem = static_cast<char*>(stage_mem);
+  if (W.rope != NONE) st->rope_tab = reinterpret_cast<float2*>(st->stage_mem + W.rope);
   if (hipGetDevice(&st->device) != hipSuccess) st->device = 0;
   *out = st;
   return RINGADA_OK;
@@ -307,7 +363,6 @@ extern "C" ringada_status ringada_stage_create(const ringada_stage_desc* desc, r
 
 extern "C" void ringada_stage_destroy(ringada_stage* st) {
   if (!st) return;
-  for (void* p : st->allocs) (void)hipFree(p);
   for (hipEvent_t e : st->evpool) (void)hipEventDestroy(e);
   delete st;
 }
@@ -315,7 +370,7 @@ extern "C" void ringada_stage_destroy(ringada_stage* st) {
 extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t block,
                                                    const ringada_block_weights* w,
                                                    const ringada_adapter* attn, const ringada_adapter* ffn,
-                                                   void* stream) {
+                                                   void* block_mem, size_t block_mem_bytes, void* stream) {
   if (!st || !w || !ffn) return fail(RINGADA_E_INVALID, "NULL argument");
   const ringada_stage_desc& D = st->D;
   const bool single = D.placement == RINGADA_PLACEMENT_FFN;
@@ -323,6 +378,11 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
     return fail(RINGADA_E_INVALID, single ? "the single placement takes no attention adapter"
                                           : "missing attention adapter");
   if (block < 0 || block >= D.n_blocks) return fail(RINGADA_E_INVALID, "block %d out of range", block);
+  if (!block_mem || block_mem_bytes < st->WL.block_bytes)
+    return fail(RINGADA_E_WORKSPACE, "block memory of %zu bytes, a block needs %zu", block_mem_bytes,
+                st->WL.block_bytes);
+  if (reinterpret_cast<uintptr_t>(block_mem) & 255u)
+    return fail(RINGADA_E_INVALID, "block memory must be 256-byte aligned");
   const bool post = D.arch == RINGADA_ARCH_POSTLN_GELU;
   if (!w->w_qkv || !w->w_o || !w->norm1_g || !w->w_in || !w->w_out || !w->norm2_g)
     return fail(RINGADA_E_INVALID, "missing frozen weight");
@@ -330,56 +390,44 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
   const bool any_post = w->b_qkv || w->b_o || w->norm1_b || w->b_in || w->b_out || w->norm2_b;
   if (post && !has_post) return fail(RINGADA_E_INVALID, "post-LN block needs every bias and beta");
   if (!post && any_post) return fail(RINGADA_E_INVALID, "pre-RMS block takes no bias or beta");
-  for (const ringada_adapter* a : {attn, ffn})
+  for (const ringada_adapter* a : {attn, ffn}) {
     if (a && (!a->w_down || !a->w_up || !a->g_down || !a->g_up))
       return fail(RINGADA_E_INVALID, "missing adapter tensor");
+    if (a && ((reinterpret_cast<uintptr_t>(a->g_down) | reinterpret_cast<uintptr_t>(a->g_up)) & 15u))
+      return fail(RINGADA_E_INVALID, "adapter gradients must be 16-byte aligned");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const int dt = D.dtype;
-  const size_t es = dt == RINGADA_BF16 ? 2 : 4;
   const size_t d = D.d_model, F = D.d_ffn, m = D.d_adapter;
+  const WeightLayout& WL = st->WL;
+  char* mem = static_cast<char*>(block_mem);
   BlockBind& b = st->blocks[block];
-  if (!b.wt_qkv) {
-    RG_TRY(dalloc(st, 3 * d * d * es, &b.wt_qkv));
-    if (st->qkv_per_head) RG_TRY(dalloc(st, 3 * d * es, &b.bqkv));
-    RG_TRY(dalloc(st, d * d * es, &b.wt_o));
-    RG_TRY(dalloc(st, (post ? 1 : 2) * F * d * es, &b.wt_in));
-    RG_TRY(dalloc(st, d * F * es, &b.wt_out));
-    for (int a = single ? 1 : 0; a < 2; ++a)
-      for (int k = 0; k < 4; ++k) RG_TRY(dalloc(st, d * m * es, &b.wk[a][k]));
-  }
-  if (!st->slots_dev) RG_TRY(dalloc(st, st->slots.size() * sizeof(AdapterSlot), (void**)&st->slots_dev));
-  if (!post && !st->rope_tab) {  // rotation angles pos * theta^(-2i/dh), in double, once per stage
+  b.wt_qkv = mem + WL.qkv;
+  b.bqkv = WL.bqkv != NONE ? mem + WL.bqkv : nullptr;
+  b.wt_o = mem + WL.o;
+  b.wt_in = mem + WL.in;
+  b.wt_out = mem + WL.out;
+  for (int a = 0; a < 2; ++a)
+    for (int k = 0; k < 4; ++k) b.wk[a][k] = WL.wk[a][k] != NONE ? mem + WL.wk[a][k] : nullptr;
+  std::vector<float2> tab;
+  if (st->rope_tab && !st->rope_built) {  // rotation angles pos * theta^(-2i/dh), in double, once per stage
     const int dh = (int)(d / D.n_heads), half = dh / 2;
-    std::vector<float2> tab((size_t)D.max_seq * half);
+    tab.resize((size_t)D.max_seq * half);
     for (int p = 0; p < D.max_seq; ++p)
       for (int i = 0; i < half; ++i) {
         const double ang = p * std::pow((double)D.rope_theta, -2.0 * i / dh);
         tab[(size_t)p * half + i] = make_float2((float)std::cos(ang), (float)std::sin(ang));
       }
-    RG_TRY(dalloc(st, tab.size() * sizeof(float2), (void**)&st->rope_tab));
-    RG_HIP(hipMemcpy(st->rope_tab, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice));
+    RG_HIP(hipMemcpyAsync(st->rope_tab, tab.data(), tab.size() * sizeof(float2), hipMemcpyHostToDevice, s));
   }
   b.w = *w;
   b.ad[0] = attn ? *attn : ringada_adapter{};
   b.ad[1] = *ffn;
-  if (st->qkv_per_head) {
-    // row (or bias element) p*d + h*dh + i of the three-block order goes to
-    // (3h + p)*dh + i
-    if (!st->qkv_tmp) RG_TRY(dalloc(st, 3 * d * d * es, &st->qkv_tmp));
-    RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), st->qkv_tmp, s));
-    const size_t dh = d / D.n_heads;
-    for (int h = 0; h < D.n_heads; ++h)
-      for (int p = 0; p < 3; ++p) {
-        const size_t src = p * d + h * dh, dst = (3 * h + p) * dh;
-        RG_HIP(hipMemcpyAsync(static_cast<char*>(b.wt_qkv) + dst * d * es,
-                              static_cast<const char*>(st->qkv_tmp) + src * d * es, dh * d * es,
-                              hipMemcpyDeviceToDevice, s));
-        RG_HIP(hipMemcpyAsync(static_cast<char*>(b.bqkv) + dst * es, static_cast<const char*>(w->b_qkv) + src * es,
-                              dh * es, hipMemcpyDeviceToDevice, s));
-      }
-  } else {
-    RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), b.wt_qkv, s));
-  }
+  // the projection transposed (in per-head row order when the stage fuses
+  // attention: row p*d + h*dh + i of the three-block order goes to (3h + p)*dh + i)
+  const int perm = st->qkv_per_head ? (int)(d / D.n_heads) : 0;
+  RG_HIP(launch_transpose(dt, dt, w->w_qkv, (int)d, (int)(3 * d), b.wt_qkv, s, perm));
+  if (b.bqkv) RG_HIP(launch_transpose(dt, dt, w->b_qkv, 1, (int)(3 * d), b.bqkv, s, perm));
   RG_HIP(launch_transpose(dt, dt, w->w_o, (int)d, (int)d, b.wt_o, s));
   if (post) RG_HIP(launch_transpose(dt, dt, w->w_in, (int)d, (int)F, b.wt_in, s));
   else RG_HIP(launch_pack_swiglu(dt, w->w_in, (int)d, (int)F, b.wt_in, s));
@@ -395,10 +443,9 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
     sl.wup = b.wk[a][2];
     sl.wup_t = b.wk[a][3];
   }
-  RG_HIP(hipMemcpyAsync(st->slots_dev + 2 * block, &st->slots[2 * block], 2 * sizeof(AdapterSlot),
-                        hipMemcpyHostToDevice, s));
-  RG_HIP(launch_adapter_sync(dt, st->slots_dev + 2 * block, 2, (int)d, (int)m, s));
-  RG_HIP(hipStreamSynchronize(s));
+  RG_HIP(launch_adapter_sync(dt, st->slots.data() + 2 * block, 2, (int)d, (int)m, s));
+  RG_HIP(hipStreamSynchronize(s));  // also keeps `tab` alive until its copy has run
+  if (st->rope_tab) st->rope_built = true;
   b.bound = true;
   return RINGADA_OK;
 }
@@ -407,7 +454,7 @@ extern "C" ringada_status ringada_stage_sync_adapters(ringada_stage* st, void* s
   if (!st) return fail(RINGADA_E_INVALID, "NULL stage");
   for (const BlockBind& b : st->blocks)
     if (!b.bound) return fail(RINGADA_E_STATE, "every block must be bound first");
-  RG_HIP(launch_adapter_sync(st->D.dtype, st->slots_dev, 2 * st->D.n_blocks, st->D.d_model,
+  RG_HIP(launch_adapter_sync(st->D.dtype, st->slots.data(), 2 * st->D.n_blocks, st->D.d_model,
                              st->D.d_adapter, static_cast<hipStream_t>(stream)));
   return RINGADA_OK;
 }
@@ -639,7 +686,9 @@ extern "C" ringada_status ringada_stage_forward(ringada_stage* st, void* stream,
   if (batch < 1 || seq < 1 || batch > D.max_batch || seq > D.max_seq)
     return fail(RINGADA_E_INVALID, "batch %d / seq %d outside [1, max]", batch, seq);
   const int c = norm_cut(lowest_unfrozen, D.n_blocks);
-  if (st->pending && c < D.n_blocks)
+  // also a frozen forward: it would run on adapters whose update is pending
+  // and overwrite the stash the pending backward reads
+  if (st->pending)
     return fail(RINGADA_E_STATE, "a forward with unfrozen adapters is pending its backward "
                                  "(one forward, one backward on unfrozen stages)");
   const size_t es = D.dtype == RINGADA_BF16 ? 2 : 4;
@@ -798,7 +847,8 @@ extern "C" ringada_status ringada_stage_backward(ringada_stage* st, void* stream
   // workgroups to fill the GPU
   const int ndw = (int)st->dw_pending.size();
   RG_TRY(run(st, cx.s, "adapter_dw", 4.0 * ndw * cx.T * cx.d * cx.m, 2.0 * ndw * cx.es * cx.T * cx.d, [&] {
-    return launch_adapter_dw_batch(cx.dt, st->dw_pending.data(), ndw, cx.s);
+    return launch_adapter_dw_batch(cx.dt, st->dw_pending.data(), ndw, static_cast<float*>(cx.W(st->L.dwp)),
+                                   (long)st->L.dwp_bytes, cx.s);
   }));
   st->pending = false;
   return RINGADA_OK;
@@ -811,13 +861,16 @@ extern "C" ringada_status ringada_adapter_step(ringada_stage* st, void* stream, 
   const ringada_stage_desc& D = st->D;
   for (int l = 0; l < D.n_blocks; ++l)
     if (!st->blocks[l].bound) return fail(RINGADA_E_STATE, "block %d is not bound", l);
+  if (st->pending)
+    return fail(RINGADA_E_STATE, "a forward is pending its backward: updating the adapters now would "
+                                 "mix new weights with the activations stashed under the old ones");
   const int c = norm_cut(lowest_unfrozen, D.n_blocks);
   const int lo = c < 0 ? 0 : c;
   if (lo >= D.n_blocks) return RINGADA_OK;
   const int n = 2 * (D.n_blocks - lo);
   const double bytes = (double)n * D.d_model * D.d_adapter * (4.0 * 4 + 4.0 * (D.dtype == RINGADA_BF16 ? 2 : 4));
   return run(st, static_cast<hipStream_t>(stream), "adapter_step", 0, bytes, [&] {
-    return launch_adapter_sgd(D.dtype, st->slots_dev + 2 * lo, n, D.d_model, D.d_adapter, opt->lr,
+    return launch_adapter_sgd(D.dtype, st->slots.data() + 2 * lo, n, D.d_model, D.d_adapter, opt->lr,
                               static_cast<hipStream_t>(stream));
   });
 }

@@ -42,9 +42,14 @@ class Stage:
         self.dev = torch.device("cuda", device)
         self.sdtype = torch.bfloat16 if w.dtype == "bf16" else torch.float32
         self.desc = make_desc(w, max_batch, max_seq)
-        self.handle = B.ringada_stage_create(self.desc)
+        # every device buffer is ours: the library's derived copies of the
+        # weights live in one region per block and one per stage
+        self.block_bytes, stage_bytes = B.ringada_stage_plan_weights(self.desc)
+        self.stage_mem = torch.empty(max(stage_bytes, 256), dtype=torch.uint8, device=self.dev)
+        self.handle = B.ringada_stage_create(self.desc, self.stage_mem, self.stage_mem.numel())
         self.frozen = []
         self.adapters = []
+        self.block_mem = []
         mp = BERT_MAP if w.arch == "bert" else LLAMA_MAP
         for l in range(w.n_blocks):
             tens = {k: self.upload(inputs["weights"][l][src]) for k, src in mp}
@@ -59,10 +64,11 @@ class Stage:
             self.adapters.append(pair)
             bw = B.BlockWeights(**{k: v.data_ptr() for k, v in tens.items()})
             ca = [B.Adapter(**{k: v.data_ptr() for k, v in t.items()}) for t in pair]
+            self.block_mem.append(torch.empty(self.block_bytes, dtype=torch.uint8, device=self.dev))
             # the single placement binds no attention adapter (its tensors
             # stay allocated here, untouched, so grads() keeps one layout)
             B.ringada_stage_bind_block(self.handle, l, bw, None if w.placement == "ffn" else ca[0], ca[1],
-                                       self.sptr)
+                                       self.block_mem[l], self.block_bytes, self.sptr)
         self.stash = self.scratch = None
         self.stash_bytes = self.scratch_bytes = 0
 

@@ -61,3 +61,54 @@ def oracle_run(w, inp, c, dy=None, x=None, batch=None, seq=None):
     out["dy"] = dy
     out["dx"], out["grads"] = O.stage_backward(desc, W, A, caches, dy, c)
     return out
+
+
+# ---------------------------------------------------------------- parity margins
+# One record per output tensor compared by a GPU parity test: the error, the
+# emulated bf16 storage floor (bf16 workloads), the bound and whether it held.
+# tests/conftest.py prints them at the end of the session and writes them to
+# gpurun_out/parity_margins.json.
+MARGINS = []
+
+
+class Checker:
+    """Compares output tensors of one GPU run with the oracle's and records
+    every margin.  bf16 workloads take, per tensor, the bound of
+    bf16_floor.floor_bound on the emulated floor `floor` (a tensor the floor
+    does not cover keeps the stated 2e-2); fp32 workloads take `tol`."""
+
+    def __init__(self, tag, floor=None, tol=None):
+        self.tag, self.floor, self.tol = tag, floor, tol
+        self.failures = []
+
+    def bound(self, key):
+        if self.tol is not None:
+            return self.tol
+        from bf16_floor import TOL_BF16, floor_bound
+        return floor_bound(self.floor, key) if self.floor and key in self.floor else TOL_BF16
+
+    def __call__(self, key, got, ref, err=None):
+        e = rel_err(got, ref) if err is None else err
+        b = self.bound(key)
+        fl = self.floor.get(key) if self.floor else None
+        MARGINS.append(dict(test=self.tag, tensor=str(key), error=e, floor=fl, bound=b, ok=bool(e <= b)))
+        print(f"[{self.tag}] {key}: error {e:.3e}" + (f", floor {fl:.3e}" if fl is not None else "")
+              + f", bound {b:.3e}" + ("" if e <= b else "  FAIL"), flush=True)
+        if not e <= b:
+            self.failures.append((key, e, b))
+        return e
+
+    def grads(self, gpu, ref, lo, L):
+        """Every adapter gradient; frozen or absent adapters must be exactly zero."""
+        for l in range(L):
+            for a in range(2):
+                for k in ("w_down", "w_up"):
+                    g = gpu[l][a][k]
+                    if l < lo or ref[l] is None or ref[l][a] is None:
+                        if not np.all(g == 0):
+                            self.failures.append(((l, a, k), "nonzero gradient of a frozen or absent adapter"))
+                        continue
+                    self((l, a, k), g, ref[l][a][k])
+
+    def done(self):
+        assert not self.failures, (self.tag, self.failures)

@@ -105,7 +105,7 @@ def test_plan_and_create_validate_arguments():
     bad = make_desc(w)
     bad.d_adapter = 48
     with pytest.raises(B.RingadaError) as e:
-        B.ringada_stage_create(bad)
+        B.ringada_stage_create(bad, None, 0)
     assert e.value.status == B.RINGADA_E_UNSUPPORTED
     bad = make_desc(w)
     bad.n_heads = 7
@@ -115,19 +115,64 @@ def test_plan_and_create_validate_arguments():
     bad = make_desc(w)
     bad.placement = 2
     with pytest.raises(B.RingadaError) as e:
-        B.ringada_stage_create(bad)
+        B.ringada_stage_create(bad, None, 0)
     assert e.value.status == B.RINGADA_E_INVALID
     bad = make_desc(WORKLOADS["llama7b_share"])
     bad.dtype = B.F32
     with pytest.raises(B.RingadaError) as e:
-        B.ringada_stage_create(bad)
+        B.ringada_stage_create(bad, None, 0)
     assert e.value.status == B.RINGADA_E_UNSUPPORTED
+
+
+def test_weight_memory_plan():
+    """The caller-owned regions for the library's derived copies: per block the
+    transposed projections (plus the per-head-order QKV bias of post-LN bf16
+    stages with d_head 64) and four working copies per adapter, each at a
+    256-B aligned offset; per stage the rotary table of the pre-RMS arch."""
+    def al(n):
+        return (n + 255) // 256 * 256
+
+    # bert_base: d 768, F 3072, m 64, bf16, per-head QKV order, two adapters
+    d, F, m = 768, 3072, 64
+    blk, stg = B.ringada_stage_plan_weights(make_desc(WORKLOADS["bert_base"]))
+    assert blk == al(3 * d * d * 2) + al(3 * d * 2) + al(d * d * 2) + 2 * al(F * d * 2) + 8 * al(d * m * 2)
+    assert blk == 14_946_816 and stg == 0
+    # single placement: one adapter's working copies fewer
+    blk1, _ = B.ringada_stage_plan_weights(make_desc(WORKLOADS["bert_base_single"]))
+    assert blk - blk1 == 4 * al(d * m * 2)
+    # llama7b_share: d 4096, SwiGLU 11008 (gate and up packed), no biases; the
+    # rotary table max_seq 512 x d_head/2 64 float pairs
+    d, F = 4096, 11008
+    blk, stg = B.ringada_stage_plan_weights(make_desc(WORKLOADS["llama7b_share"]))
+    assert blk == al(3 * d * d * 2) + al(d * d * 2) + al(2 * F * d * 2) + al(F * d * 2) + 8 * al(d * m * 2)
+    assert stg == 512 * 64 * 8
+    # the tiny fp32 stage: 4-byte elements, no per-head order
+    d, F, m = 128, 512, 16
+    blk, stg = B.ringada_stage_plan_weights(make_desc(WORKLOADS["tiny"]))
+    assert blk == al(3 * d * d * 4) + al(d * d * 4) + 2 * al(F * d * 4) + 8 * al(d * m * 4)
+    assert stg == 0
+
+
+def test_create_checks_the_stage_memory():
+    desc = make_desc(WORKLOADS["llama7b_share"])
+    _, stg = B.ringada_stage_plan_weights(desc)
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_create(desc, None, 0)
+    assert e.value.status == B.RINGADA_E_WORKSPACE
+    with pytest.raises(B.RingadaError) as e:
+        B.ringada_stage_create(desc, 1 << 20, stg - 1)
+    assert e.value.status == B.RINGADA_E_WORKSPACE
+    with pytest.raises(B.RingadaError) as e:  # 256-B alignment
+        B.ringada_stage_create(desc, (1 << 20) + 16, stg)
+    assert e.value.status == B.RINGADA_E_INVALID
+    h = B.ringada_stage_create(desc, 1 << 20, stg)  # host-side only: the address is not touched
+    B.ringada_stage_destroy(h)
 
 
 def test_state_machine_on_an_unbound_stage():
     """Calls out of order fail with E_STATE before touching the device."""
     w = WORKLOADS["tiny"]
-    h = B.ringada_stage_create(make_desc(w))
+    h = B.ringada_stage_create(make_desc(w), None, 0)
     try:
         with pytest.raises(B.RingadaError) as e:
             B.ringada_stage_forward(h, None, 16, 4096, w.batch, w.seq, 0, 0, 0, 0, 0)
