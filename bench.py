@@ -45,6 +45,21 @@ def kernel_source_hash(name):
     return h.hexdigest()
 
 
+def recorded_trace_us(name, workload):
+    """Average duration (us) of kernel `name` in the committed rocprofv3 kernel
+    trace of `workload`, if one exists and was taken on the current sources of
+    that kernel; else None."""
+    path = os.path.join(ROOT, "profiles", f"kernel_trace_{workload}.md")
+    if not os.path.exists(path):
+        return None
+    want = kernel_source_hash(name)
+    for line in open(path):
+        m = re.match(r"\s*trace:\s+kernel=(\S+)\s+avg_us=([0-9.]+)\s+source_sha256=([0-9a-f]+)", line)
+        if m and m.group(1) == name and m.group(3) == want:
+            return float(m.group(2))
+    return None
+
+
 def recorded_traffic(name, workload):
     """HBM bytes per launch of kernel `name` on `workload`, from the committed
     rocprofv3 FETCH_SIZE / WRITE_SIZE summary, if one exists and was taken on
@@ -114,7 +129,8 @@ def cpu_baseline(w, inp, min_seconds=10.0, max_steps=8):
         steps += 1
     dt = time.perf_counter() - t0
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    return {"value": round(steps * w.batch / dt, 3), "unit": "samples/s", "cores": int(threads), "kind": "oracle",
+    return {"value": round(steps * w.batch / dt, 3), "unit": "samples/s", "cores": len(os.sched_getaffinity(0)),
+            "blas_threads": int(threads), "kind": "oracle", "impl": "numpy float64 oracle (tests' reference)",
             "sample": f"{steps} full step(s) (forward, head loss, backward to block {w.lowest_unfrozen}, SGD) of "
                       f"the {w.name} workload, all {w.batch} samples each, numpy float64 oracle, {dt:.2f} s"}
 
@@ -234,6 +250,10 @@ def main():
     gemms = [e for e in prof if e["name"].startswith(GEMM_PREFIX)]
     gemm_flops = sum(e["flops"] for e in gemms)
     gemm_ms = sum(e["total_ms"] for e in gemms)
+    # the projection FLOPs alone: the fused QKV projection + attention kernel also
+    # counts the attention's 4 B H S^2 d_head per launch, which is not GEMM work
+    attn_in_gemm = sum(e["launches"] * 4.0 * w.batch * w.n_heads * w.seq * w.seq * (w.d_model // w.n_heads)
+                       for e in gemms if e["name"] == "gemm_qkv_attn_fwd")
     all_flops = sum(e["flops"] for e in prof)
     dom = prof[0]
     dom_avg_s = dom["total_ms"] * 1e-3 / dom["launches"]
@@ -249,6 +269,12 @@ def main():
                 "avg_us": round(dom_avg_s * 1e6, 2), "launches_per_step": dom["launches"] // args.steps}
 
     roof["traffic"] = recorded_traffic(dom["name"], w.name)
+    # the same kernel's average duration in the committed rocprofv3 kernel trace
+    # (null if its sources changed since), and the fraction that duration gives
+    traced = recorded_trace_us(dom["name"], w.name)
+    roof["traced_avg_us"] = traced
+    roof["frac_traced"] = (round(dom["flops" if roof["bound"] == "mfma" else "bytes"] / dom["launches"] / (traced * 1e-6)
+                                 / (1e12 if roof["bound"] == "mfma" else 1e9) / roof["peak"], 4) if traced else None)
     cpu = None if args.no_cpu_baseline else cpu_baseline(w, inp)
     st.close()
     if args.copy_calib_mib:
@@ -265,7 +291,9 @@ def main():
                    "placement": w.placement,
                    "parallelism": "one ring stage on one GPU"},
         "tokens_per_s": round(value * w.seq, 1),
-        "gemm_mfma_frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
+        "gemm_mfma_frac": (round((gemm_flops - attn_in_gemm) / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4)
+                           if gemm_ms else None),
+        "gemm_attn_mfma_frac": round(gemm_flops / (gemm_ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4) if gemm_ms else None,
         "stage_mfma_frac": round(all_flops / args.steps / (ms * 1e-3) / 1e12 / PEAK_BF16_TFLOPS, 4),
         "stash_bytes": stash_bytes, "scratch_bytes": scratch_bytes,
         "launch": "hip_graph" if run is not step else "eager",
