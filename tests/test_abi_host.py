@@ -102,6 +102,10 @@ def test_plan_and_create_validate_arguments():
     with pytest.raises(B.RingadaError) as e:
         B.ringada_stage_plan(desc, w.batch + 1, w.seq, 8)
     assert e.value.status == B.RINGADA_E_INVALID
+    for batch, seq in ((0, w.seq), (w.batch, 0), (-1, 1)):  # empty or negative sizes
+        with pytest.raises(B.RingadaError) as e:
+            B.ringada_stage_plan(desc, batch, seq, 8)
+        assert e.value.status == B.RINGADA_E_INVALID
     bad = make_desc(w)
     bad.d_adapter = 48
     with pytest.raises(B.RingadaError) as e:

@@ -63,6 +63,15 @@ SMALL = {
                                       "dy", 2014),
     # the bidirectional multi-tile path on a ragged length (three key tiles)
     "small_bert_s300": Workload("small_bert_s300", "bert", "bf16", 2, 256, 4, 512, 64, 300, 2, 0, "dy", 2015),
+    # degenerate shapes: one-token sequences (attention over a single key is V
+    # itself; the rotary angle at position 0 is zero), fewer tokens than one
+    # 16-token row tile or one GEMM row tile, the wide adapter path on 3 tokens
+    "edge_bert_s1": Workload("edge_bert_s1", "bert", "bf16", 2, 256, 4, 512, 64, 1, 3, 0, "dy", 2016),
+    "edge_llama_s1": Workload("edge_llama_s1", "llama", "bf16", 2, 256, 2, 384, 64, 1, 2, 1, "dy", 2017),
+    "edge_bert_t5": Workload("edge_bert_t5", "bert", "bf16", 2, 256, 4, 512, 64, 5, 1, 1, "dy", 2018),
+    "edge_tiny_s1_f32": Workload("edge_tiny_s1_f32", "bert", "f32", 2, 128, 2, 512, 16, 1, 2, 0, "dy", 2019,
+                                 tiny_adapter_init=True),
+    "edge_wide_llama_t3": Workload("edge_wide_llama_t3", "llama", "bf16", 2, 2048, 16, 512, 64, 3, 1, 0, "dy", 2020),
 }
 
 
