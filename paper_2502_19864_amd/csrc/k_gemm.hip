@@ -931,17 +931,50 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
   } else {
     return hipErrorInvalidValue;
   }
-  switch (role) {
-    case R_QKV_FWD: return launch_epi<R_QKV_FWD>(epi, cfg, dtype, a, s);
-    case R_O_FWD: return launch_epi<R_O_FWD>(epi, cfg, dtype, a, s);
-    case R_FFN_IN_FWD: return launch_epi<R_FFN_IN_FWD>(epi, cfg, dtype, a, s);
-    case R_FFN_OUT_FWD: return launch_epi<R_FFN_OUT_FWD>(epi, cfg, dtype, a, s);
-    case R_QKV_DX: return launch_epi<R_QKV_DX>(epi, cfg, dtype, a, s);
-    case R_O_DX: return launch_epi<R_O_DX>(epi, cfg, dtype, a, s);
-    case R_FFN_IN_DX: return launch_epi<R_FFN_IN_DX>(epi, cfg, dtype, a, s);
-    case R_FFN_OUT_DX: return launch_epi<R_FFN_OUT_DX>(epi, cfg, dtype, a, s);
-    default: return hipErrorInvalidValue;
+  auto go = [&](Cfg c, const GemmArgs& g) -> hipError_t {
+    switch (role) {
+      case R_QKV_FWD: return launch_epi<R_QKV_FWD>(epi, c, dtype, g, s);
+      case R_O_FWD: return launch_epi<R_O_FWD>(epi, c, dtype, g, s);
+      case R_FFN_IN_FWD: return launch_epi<R_FFN_IN_FWD>(epi, c, dtype, g, s);
+      case R_FFN_OUT_FWD: return launch_epi<R_FFN_OUT_FWD>(epi, c, dtype, g, s);
+      case R_QKV_DX: return launch_epi<R_QKV_DX>(epi, c, dtype, g, s);
+      case R_O_DX: return launch_epi<R_O_DX>(epi, c, dtype, g, s);
+      case R_FFN_IN_DX: return launch_epi<R_FFN_IN_DX>(epi, c, dtype, g, s);
+      case R_FFN_OUT_DX: return launch_epi<R_FFN_OUT_DX>(epi, c, dtype, g, s);
+      default: return hipErrorInvalidValue;
+    }
+  };
+  // The 256x128 kernel runs one workgroup per CU.  When its tiles leave the
+  // GPU's last round at most half full (LLaMA-7B FFN-in: 8 x 172 = 1376 tiles,
+  // five rounds of 256 and 96), that round is split off along N: the columns
+  // of the whole rounds go to this kernel, the rest to 128x128 tiles, which
+  // spread it over every CU instead of leaving most of them idle.  Each output
+  // column is still computed by one tile, in the same order.
+  if (cfg == C_P256x128_8W && !rope) {
+    const int rt = (a.M + 255) / 256;
+    const long nt = (long)rt * ((a.N + 127) / 128), rem = nt % 256;
+    if (256 % rt == 0 && rem != 0 && rem <= 128) {
+      const int n_main = (int)(nt / 256) * (256 / rt) * 128;
+      if (n_main > 0 && n_main < a.N) {
+        GemmArgs m = a, t = a;
+        m.N = n_main;
+        t.N = a.N - n_main;
+        t.B = static_cast<const bf16*>(a.B) + (long)n_main * a.ldb;
+        // output columns: SwiGLU writes one column per gate/up pair (the stash
+        // keeps the pair at f and half + f); every other epilogue one per column
+        const int oc = epi == Epi::SwiGlu ? n_main / 2 : n_main;
+        t.out = static_cast<bf16*>(a.out) + oc;
+        if (a.out2) t.out2 = static_cast<bf16*>(a.out2) + oc;
+        if (a.bias) t.bias = static_cast<const bf16*>(a.bias) + n_main;
+        if (a.aux) t.aux = static_cast<const bf16*>(a.aux) + n_main;
+        const long tail_tiles = (long)((a.M + 127) / 128) * ((t.N + 127) / 128);
+        const Cfg ct = tail_tiles >= 512 ? C_P128x128_2 : C_P128x128_3;
+        const hipError_t e = go(cfg, m);
+        return e != hipSuccess ? e : go(ct, t);
+      }
+    }
   }
+  return go(cfg, a);
 }
 
 }  // namespace rg
