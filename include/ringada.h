@@ -113,7 +113,9 @@ typedef struct {
 /* One adapter of Eq. (1) (no biases): fp32 master weights and fp32 gradient
  * accumulators, device, caller-owned, borrowed until ringada_stage_destroy.
  * The backward ADDS into g_down/g_up; ringada_adapter_step consumes and zeroes
- * them. */
+ * them.  g_down and g_up must be 16-byte aligned (ringada_stage_bind_block
+ * returns RINGADA_E_INVALID otherwise); the bf16 backward sums each gradient
+ * element in a fixed order, so equal inputs give bitwise equal gradients. */
 typedef struct {
   float* w_down; /* [d, m] */
   float* w_up;   /* [m, d] */
