@@ -345,8 +345,14 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     float sum = 0.f;
 #pragma unroll
     for (int k2 = 0; k2 < KS; ++k2) sum += sPart[(k2 * MB + unit) * TOKP + wave];
-    const bf16 du = f2bf(sum * gelu_grad_fast(bf2f(uraw)));
+    // gelu'(U) for dU and, when asked for, gelu(U) for the weight gradient of
+    // W_up, from one erf evaluation (the same bits as gelu_fast / gelu_grad_fast)
+    const float uf = bf2f(uraw);
+    const ErfGauss eg = erf_gauss_as(uf);
+    const float phi2 = 1.f + eg.erf_z;
+    const bf16 du = f2bf(sum * fmaf(uf * 0.39894228040143268f, eg.gauss, 0.5f * phi2));
     if (twv) static_cast<bf16*>(a.du)[(long)tw * MB + unit] = du;
+    if (a.gu && twv) static_cast<bf16*>(a.gu)[(long)tw * MB + unit] = f2bf(0.5f * uf * phi2);
     sdU[wave * GP + unit] = du;
   }
   if (!a.dzin) return;
@@ -418,7 +424,10 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
   const AdapterDwArgs& a = batch.a[bz >> 1];
   const bool up = (bz & 1) == 0;
   const int d = a.d, T = a.T;
-  const bf16* X = static_cast<const bf16*>(up ? a.u : a.z);
+  // dW_up's operand is gelu(U): read as the adapter backward formed it, or
+  // formed here from U by every column tile of the chunk
+  const bool form_gelu = up && !a.gu;
+  const bf16* X = static_cast<const bf16*>(up ? (a.gu ? a.gu : a.u) : a.z);
   const bf16* Y = static_cast<const bf16*>(up ? a.dz : a.du);
   const int ldx = up ? MB : d, ldy = up ? d : MB;
   const int ldc = up ? d : MB;
@@ -448,7 +457,7 @@ __global__ __launch_bounds__(256) void adapter_dw_bf16(AdapterDwBatch batch) {
     for (int i = 0; i < 2; ++i) {
       const int idx = tid + i * 256, tt = idx / 8, c = idx % 8;
       bf16x8 xv = xr[sb][i];
-      if (up) {
+      if (form_gelu) {
         float f[8];
         unpack_frag(xv, f);
 #pragma unroll
@@ -910,6 +919,11 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
   return hipGetLastError();
 }
 
+bool adapter_bwd_forms_gelu(int dtype, int d) {
+  int nw, fb;
+  return dtype == DT_BF16 && bf16_shape(d, nw, fb) && fb <= 4;  // the one-kernel backward
+}
+
 hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s) {
   // an absent adapter (both weight pointers NULL): only the norm backward, into dz
   const bool has_ad = a.wup || a.wdn;
@@ -919,6 +933,7 @@ hipError_t launch_adapter_bwd(int dtype, const AdapterBwdArgs& a, hipStream_t s)
   if (!a.dz && a.norm != Norm::None) return hipErrorInvalidValue;
   if (a.norm != Norm::None && (!a.xhat || !a.rstd || !a.gamma)) return hipErrorInvalidValue;
   if (a.norm == Norm::RMS && !a.dres) return hipErrorInvalidValue;
+  if (a.gu && (!has_ad || !adapter_bwd_forms_gelu(dtype, a.d))) return hipErrorInvalidValue;
   if (a.T == 0) return hipSuccess;
   if (dtype == DT_BF16) {
     int nw, fb;
@@ -951,6 +966,7 @@ hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, flo
   for (int k = 0; k < n; ++k) {
     const AdapterDwArgs& x = a[k];
     if (x.T < 0 || !x.u || !x.dz || !x.z || !x.du || !x.g_up || !x.g_down) return hipErrorInvalidValue;
+    if (x.gu && dtype != DT_BF16) return hipErrorInvalidValue;  // the fp32 kernel forms gelu(U) itself
   }
   if (n == 0 || a[0].T == 0) return hipSuccess;
   if (dtype != DT_BF16) {
@@ -965,7 +981,7 @@ hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, flo
   for (int k = 0; k < n; ++k) {
     const AdapterDwArgs& x = a[k];
     if (x.T != a[0].T || x.d != a[0].d || x.m != a[0].m || x.m != MB || x.d % 64) return hipErrorInvalidValue;
-    if (!al16(x.g_up) || !al16(x.g_down)) return hipErrorInvalidValue;
+    if (!al16(x.g_up) || !al16(x.g_down) || (x.gu && !al16(x.gu))) return hipErrorInvalidValue;
   }
   if (!part || !al16(part) || part_bytes < adapter_dw_part_bytes(dtype, a[0].T, a[0].d, a[0].m, n))
     return hipErrorInvalidValue;

@@ -139,6 +139,9 @@ struct AdapterBwdArgs {
   void* dz;           // gradient at the adapter output [T, d]; may be null for
                       // Norm::None (it equals gin)
   void* du;           // gradient at z W_down [T, m] (always written)
+  void* gu;           // gelu(U) [T, m] as bf16, the weight-gradient operand of
+                      // W_up; null = not formed (adapter_bwd_forms_gelu says
+                      // which shapes can form it)
   void* dzin;         // gradient at the adapter input [T, d]; null = skip
   float* part;        // bf16 with d > 1024: fp32 scratch [d / 1024][T][m] for the
                       // split-K partial sums of dZ W_up^T; unused otherwise
@@ -156,7 +159,12 @@ struct AdapterDwArgs {
   const void* du;  // [T, m]
   float* g_up;     // [m, d]
   float* g_down;   // [d, m]
+  const void* gu;  // gelu(U) [T, m] when the adapter backward formed it, else
+                   // null (then formed here from u)
 };
+// whether launch_adapter_bwd can also write gelu(U) (AdapterBwdArgs::gu) for
+// this storage type and width: bf16 up to d = 1024
+bool adapter_bwd_forms_gelu(int dtype, int d);
 // bytes of the fp32 per-chunk partial sums launch_adapter_dw_batch needs for
 // n adapters (0 for fp32 stages)
 long adapter_dw_part_bytes(int dtype, int T, int d, int m, int n_adapters);

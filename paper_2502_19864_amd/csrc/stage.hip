@@ -70,6 +70,10 @@ struct Layout {
   // gradients at its output (dz) and at z W_down (du), kept until the one
   // weight-gradient launch at the end of the backward
   std::vector<size_t> gdz, gdu;
+  // and gelu(U), the W_up weight-gradient operand, where the adapter backward
+  // forms it (bf16 up to d = 1024; else NONE and the weight-gradient launch
+  // forms it from the stashed U)
+  std::vector<size_t> ggu;
   size_t adp;  // both passes
   // per-chunk partial sums of the weight-gradient launch at the end of the
   // backward; they take the place of the backward's temporaries, all dead by
@@ -163,12 +167,15 @@ static void plan_layout(const ringada_stage_desc& D, int B, int S, int c, Layout
   const size_t temporaries = cur;
   L.gdz.assign(2 * D.n_blocks, NONE);
   L.gdu.assign(2 * D.n_blocks, NONE);
+  L.ggu.assign(2 * D.n_blocks, NONE);
+  const bool form_gelu = adapter_bwd_forms_gelu(D.dtype == RINGADA_BF16 ? DT_BF16 : DT_F32, (int)d);
   int n_dw = 0;
   for (int l = 0; l < D.n_blocks; ++l) {
     if (block_kind(l, c, D.n_blocks) == K_NONE) continue;
     for (int a = single ? 1 : 0; a < 2; ++a) {
       L.gdz[2 * l + a] = take(Td);
       L.gdu[2 * l + a] = take(Tm);
+      if (form_gelu) L.ggu[2 * l + a] = take(Tm);
       ++n_dw;
     }
   }
@@ -735,7 +742,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   // FFN adapter (+ LN2 for post-LN)
   AdapterBwdArgs ab{};
   ab.T = T; ab.d = d; ab.m = m; ab.gin = G; ab.u = c.S(sb.u2);
-  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = c.W(L.gdu[2 * l + 1]);
+  ab.wup = b.wk[1][2]; ab.wdn = b.wk[1][0]; ab.du = c.W(L.gdu[2 * l + 1]); ab.gu = c.W(L.ggu[2 * l + 1]);
   ab.dzin = stop_ffn ? nullptr : c.W(L.df2);
   ab.part = static_cast<float*>(c.W(L.adp));
   // the gradient at the adapter output goes to this adapter's own buffer
@@ -751,7 +758,8 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   RG_TRY(run(st, c.s, "adapter_bwd", stop_ffn ? 4.0 * T * d * m : ad_flops,
              es * ((c.llama ? 3.0 : 5.0) - (stop_ffn ? 1.0 : 0.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, ab, c.s); }));
-  st->dw_pending.push_back(AdapterDwArgs{T, d, m, c.S(sb.u2), dz2, c.S(sb.f2), ab.du, b.ad[1].g_up, b.ad[1].g_down});
+  st->dw_pending.push_back(
+      AdapterDwArgs{T, d, m, c.S(sb.u2), dz2, c.S(sb.f2), ab.du, b.ad[1].g_up, b.ad[1].g_down, ab.gu});
   if (stop_ffn) return RINGADA_OK;
 
   // FFN (dX only through frozen weights)
@@ -774,6 +782,7 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
   aa.part = static_cast<float*>(c.W(L.adp));
   if (!single) {
     aa.u = c.S(sb.u1); aa.wup = b.wk[0][2]; aa.wdn = b.wk[0][0]; aa.du = c.W(L.gdu[2 * l]);
+    aa.gu = c.W(L.ggu[2 * l]);
     aa.dzin = stop ? nullptr : c.W(L.dattn);
   }
   void* dattn = single ? dz1 : c.W(L.dattn);
@@ -788,7 +797,8 @@ static ringada_status block_backward(const Ctx& c, int l, const void* G, void* d
              es * ((c.llama ? 4.0 : 3.0) + (stop || single ? 0.0 : 1.0)) * T * d,
              [&] { return launch_adapter_bwd(c.dt, aa, c.s); }));
   if (!single)
-    st->dw_pending.push_back(AdapterDwArgs{T, d, m, c.S(sb.u1), dz1, c.S(sb.attn), aa.du, b.ad[0].g_up, b.ad[0].g_down});
+    st->dw_pending.push_back(
+        AdapterDwArgs{T, d, m, c.S(sb.u1), dz1, c.S(sb.attn), aa.du, b.ad[0].g_up, b.ad[0].g_down, aa.gu});
   if (stop) return RINGADA_OK;
 
   // attention (dX only)
