@@ -5,10 +5,11 @@
 // bf16: MFMA 32x32x16 with large per-wave tiles, operands moved global -> LDS
 // by DMA in a multi-stage pipeline, fragment reads overlapped with the MFMAs,
 // and an epilogue that stages the output tile through LDS so that every
-// global access is a whole-row 16-B vector (gemm_bf16_pipe_body).  A
-// register-staged variant (gemm_bf16_body) covers the shapes the pipelined
-// kernel does not take.  The MFMA computes C^T blocks so that each lane owns
-// four consecutive output columns of one row.
+// global access is a whole-row 16-B vector (gemm_bf16_pipe_body).  It takes
+// every shape of a bf16 stage (K a multiple of 64: d a multiple of 256, the
+// FFN width of 64; 16-B aligned operands); others are refused.  The MFMA
+// computes C^T blocks so that each lane owns four consecutive output columns
+// of one row.
 // f32: a plain FMA tile kernel (used by the small fp32 stage only).
 #include <type_traits>
 
@@ -21,62 +22,32 @@
 namespace rg {
 
 // ---------------------------------------------------------------- epilogues
-template <Epi E, typename T>
-__device__ __forceinline__ void epilogue4(const GemmArgs& a, int m, int n, float v[4]) {
+// fp32 epilogue on four consecutive output columns n..n+3 of row m (the fp32
+// path is the post-LN block only: store + bias, GELU, residual, GELU')
+template <Epi E>
+__device__ __forceinline__ void epilogue4_f32(const GemmArgs& a, int m, int n, float v[4]) {
+  static_assert(E == Epi::Store || E == Epi::Gelu || E == Epi::Resid || E == Epi::DGelu,
+                "post-LN epilogues only");
   const long r = m;
   if constexpr (E == Epi::Store || E == Epi::Gelu) {
     if (a.bias) {
       float b[4];
-      St<T>::ld4(static_cast<const T*>(a.bias), n, b);
+      St<float>::ld4(static_cast<const float*>(a.bias), n, b);
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[i] += b[i];
     }
     if constexpr (E == Epi::Gelu) {
-      if (a.out2) St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + n, v);
+      if (a.out2) St<float>::st4(static_cast<float*>(a.out2), r * a.ldo2 + n, v);
 #pragma unroll
-      for (int i = 0; i < 4; ++i) v[i] = std::is_same_v<T, float> ? gelu_f(v[i]) : gelu_fast(v[i]);
+      for (int i = 0; i < 4; ++i) v[i] = gelu_f(v[i]);
     }
-    St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, v);
-  } else if constexpr (E == Epi::Resid) {
+  } else {
     float x[4];
-    St<T>::ld4(static_cast<const T*>(a.aux), r * a.ld_aux + n, x);
+    St<float>::ld4(static_cast<const float*>(a.aux), r * a.ld_aux + n, x);
 #pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] += x[i];
-    St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, v);
-  } else if constexpr (E == Epi::DGelu) {
-    float x[4];
-    St<T>::ld4(static_cast<const T*>(a.aux), r * a.ld_aux + n, x);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] *= std::is_same_v<T, float> ? gelu_grad_f(x[i]) : gelu_grad_fast(x[i]);
-    St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, v);
-  } else if constexpr (E == Epi::DSwiGlu) {
-    float g[4], u[4], dg[4], du[4];
-    St<T>::ld4(static_cast<const T*>(a.aux), r * a.ld_aux + n, g);
-    St<T>::ld4(static_cast<const T*>(a.aux), r * a.ld_aux + a.half + n, u);
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float sg = sigmoid_f(g[i]);
-      du[i] = v[i] * g[i] * sg;
-      dg[i] = v[i] * u[i] * (sg + g[i] * sg * (1.f - sg));
-    }
-    St<T>::st4(static_cast<T*>(a.out), r * a.ldo + n, dg);
-    St<T>::st4(static_cast<T*>(a.out), r * a.ldo + a.half + n, du);
+    for (int i = 0; i < 4; ++i) v[i] = E == Epi::Resid ? v[i] + x[i] : v[i] * gelu_grad_f(x[i]);
   }
-}
-
-// gate/up pair for feature columns f..f+3
-template <typename T>
-__device__ __forceinline__ void epilogue_swiglu4(const GemmArgs& a, int m, int f, const float g[4],
-                                                 const float u[4]) {
-  const long r = m;
-  float o[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) o[i] = g[i] * sigmoid_f(g[i]) * u[i];
-  St<T>::st4(static_cast<T*>(a.out), r * a.ldo + f, o);
-  if (a.out2) {
-    St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + f, g);
-    St<T>::st4(static_cast<T*>(a.out2), r * a.ldo2 + a.half + f, u);
-  }
+  St<float>::st4(static_cast<float*>(a.out), r * a.ldo + n, v);
 }
 
 // eight consecutive bf16 (16-B aligned) <-> float
@@ -145,131 +116,6 @@ __device__ __forceinline__ void epilogue_swiglu8(const GemmArgs& a, int m, int f
   if (a.out2) {
     st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + f, g);
     st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + a.half + f, u);
-  }
-}
-
-// ---------------------------------------------------------------- bf16 MFMA kernel
-constexpr int BK = 64;
-constexpr int LDK = BK + 8;  // LDS row pitch (bf16): 144 B keeps 16-B fragment reads conflict-free
-
-template <int BM, int BN, int WM, int WN, Epi E>
-__device__ __forceinline__ void gemm_bf16_body(const GemmArgs& a) {
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int CPR = BK / 8;  // 16-B chunks per tile row
-  constexpr int AC = BM * CPR / 256, BC = BN * CPR / 256;
-  static_assert(WM * WN == 4, "four waves");
-  static_assert(AC * 256 == BM * CPR && BC * 256 == BN * CPR, "tile/thread mismatch");
-  static_assert(E != Epi::SwiGlu || FN % 2 == 0, "SwiGlu needs gate/up block pairs");
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * LDK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * LDK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-  const int m0 = blockIdx.y * BM, n0 = blockIdx.x * BN;
-  const bf16* A = static_cast<const bf16*>(a.A);
-  const bf16* B = static_cast<const bf16*>(a.B);
-  const int M = a.M, N = a.N, K = a.K;
-
-  uint4 ra[AC], rb[BC];
-  auto gload = [&](int k0) {
-#pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      int idx = tid + i * 256, r = idx / CPR, c = idx % CPR;
-      int gm = m0 + r, gk = k0 + c * 8;
-      ra[i] = (gm < M && gk < K) ? *reinterpret_cast<const uint4*>(A + (long)gm * a.lda + gk)
-                                 : make_uint4(0, 0, 0, 0);
-    }
-#pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      int idx = tid + i * 256, r = idx / CPR, c = idx % CPR;
-      int gn = n0 + r, gk = k0 + c * 8;
-      rb[i] = (gn < N && gk < K) ? *reinterpret_cast<const uint4*>(B + (long)gn * a.ldb + gk)
-                                 : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto sstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < AC; ++i) {
-      int idx = tid + i * 256, r = idx / CPR, c = idx % CPR;
-      *reinterpret_cast<uint4*>(&sA[buf][r * LDK + c * 8]) = ra[i];
-    }
-#pragma unroll
-    for (int i = 0; i < BC; ++i) {
-      int idx = tid + i * 256, r = idx / CPR, c = idx % CPR;
-      *reinterpret_cast<uint4*>(&sB[buf][r * LDK + c * 8]) = rb[i];
-    }
-  };
-
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.f;
-
-  const int nk = (K + BK - 1) / BK;
-  gload(0);
-  sstore(0);
-  __syncthreads();
-  const int lrow = lane & 31, lk = (lane >> 5) * 8;
-  for (int kt = 0; kt < nk; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < nk) gload((kt + 1) * BK);
-    const bf16* pa = &sA[cur][(wm * TM + lrow) * LDK + lk];
-    const bf16* pb = &sB[cur][(wn * TN + lrow) * LDK + lk];
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 fa[FM], fb[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) fa[i] = ld_frag(pa + i * 32 * LDK + ks * 16);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) fb[j] = ld_frag(pb + j * 32 * LDK + ks * 16);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma32(fb[j], fa[i], acc[i][j]);
-    }
-    if (kt + 1 < nk) sstore(cur ^ 1);
-    __syncthreads();
-  }
-
-  // lane owns row m = m0 + wm*TM + i*32 + lane%32 and, per group g, columns
-  // n0 + wn*TN + j*32 + 8g + 4*(lane/32) + {0..3}
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-    const int m = m0 + wm * TM + i * 32 + lrow;
-    if (m >= M) continue;
-    if constexpr (E == Epi::SwiGlu) {
-#pragma unroll
-      for (int j = 0; j < FN; j += 2) {
-        // packed columns [64p, 64p+32) are gates, [64p+32, 64p+64) the matching ups
-        const int ng = n0 + wn * TN + j * 32;
-        if (ng >= N) continue;
-        const int fbase = (ng / 64) * 32;
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          float gv[4], uv[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) { gv[q] = acc[i][j][4 * g + q]; uv[q] = acc[i][j + 1][4 * g + q]; }
-          epilogue_swiglu4<bf16>(a, m, fbase + 8 * g + 4 * (lane >> 5), gv, uv);
-        }
-      }
-    } else {
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-#pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int n = n0 + wn * TN + j * 32 + 8 * g + 4 * (lane >> 5);
-          if (n >= N) continue;
-          float v[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) v[q] = acc[i][j][4 * g + q];
-          epilogue4<E, bf16>(a, m, n, v);
-        }
-      }
-    }
   }
 }
 
@@ -706,7 +552,7 @@ __device__ __forceinline__ void gemm_f32_body(const GemmArgs& a) {
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
     const int m = m0 + ty * 4 + i, n = n0 + tx * 4;
-    if (m < a.M && n < a.N) epilogue4<E, float>(a, m, n, acc[i]);
+    if (m < a.M && n < a.N) epilogue4_f32<E>(a, m, n, acc[i]);
   }
 }
 
@@ -714,10 +560,6 @@ __device__ __forceinline__ void gemm_f32_body(const GemmArgs& a) {
 // Two-stage 4-wave tiles run two workgroups per CU (LDS <= 80 KB), so their
 // registers must fit two waves per SIMD; the bound says so to the compiler.
 #define RG_GEMM_KERNELS(NAME)                                                        \
-  template <int BM, int BN, int WM, int WN, Epi E>                                   \
-  __global__ __launch_bounds__(256) void NAME(GemmArgs a) {                          \
-    gemm_bf16_body<BM, BN, WM, WN, E>(a);                                            \
-  }                                                                                  \
   template <int BM, int BN, int WM, int WN, int NS, Epi E>                           \
   __global__ __launch_bounds__(256, NS == 2 ? 2 : 1) void NAME##_pipe(GemmArgs a) {  \
     gemm_bf16_pipe_body<BM, BN, WM, WN, 64, NS, E, 4>(a);                            \
@@ -771,9 +613,32 @@ static constexpr bool role_has(Role r, Epi e) {
 //    CU) from two tiles per CU on, three stages below.
 // The SwiGLU epilogues take only the 64-wide wave tiles (a gate/up block pair
 // per wave): 256x128 or 128x128.
-// The register staged kernel covers K % 64 != 0 and unaligned epilogue operands.
-enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_P256x192_8W, C_P256x128_8W, C_REG_128x128,
-           C_REG_64x128 };
+enum Cfg { C_P128x192, C_P128x96, C_P128x128_2, C_P128x128_3, C_P256x192_8W, C_P256x128_8W };
+
+// The (role, epilogue, tile) kernels that launch_gemm can select for a stage,
+// the only ones instantiated.  Besides what role_has excludes:
+//  - the gated and rotary epilogues take only the 64-wide wave tiles;
+//  - the QKV-dX GEMM has K = 3N, so N divisible by 192 (N = d a multiple of
+//    256) means K > 1024, past the 128x192 tile's K limit;
+//  - the QKV projection's output (N = 3d) is a multiple of 192, so it takes
+//    128x192 (K <= 1024) or an 8-wave tile (K > 1024) whenever the tiles
+//    would fill two workgroups per CU on 128x128; its 128x128 tiles are the
+//    three-stage ones.
+static constexpr bool cfg_has(Role R, Epi E, Cfg c) {
+  const bool glu = E == Epi::SwiGlu || E == Epi::DSwiGlu || E == Epi::Rope;
+  switch (c) {
+    case C_P128x192: return !glu && R != R_QKV_DX;
+    case C_P128x96: case C_P256x192_8W: return !glu;
+    case C_P128x128_2: return !(R == R_QKV_FWD && E == Epi::Store);
+    default: return true;
+  }
+}
+// fp32 stages are post-LN only: no gated or rotary epilogue, and the dX
+// GEMMs of the QKV and FFN-in projections add the residual
+static constexpr bool f32_has(Role R, Epi E) {
+  return E == Epi::Store ? (R != R_QKV_DX && R != R_FFN_IN_DX)
+                         : (E == Epi::Gelu || E == Epi::Resid || E == Epi::DGelu);
+}
 
 template <Role R, Epi E>
 static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t s) {
@@ -786,67 +651,47 @@ static hipError_t launch_role(Cfg cfg, int dtype, const GemmArgs& a, hipStream_t
       return hipGetLastError();
     } else {
     if (dtype == DT_F32) {
-      if constexpr (E == Epi::SwiGlu || E == Epi::Rope) return hipErrorInvalidValue;
+      if constexpr (!f32_has(R, E)) return hipErrorInvalidValue;
       else {
         dim3 grid((a.N + 63) / 64, (a.M + 63) / 64);
-        switch (R) {
-#define RG_F32(ROLE, NAME) case ROLE: RG_LAUNCH((NAME##_f32<E>), grid, block, 0, s, a); break;
-          RG_F32(R_QKV_FWD, gemm_qkv_fwd) RG_F32(R_O_FWD, gemm_o_fwd) RG_F32(R_FFN_IN_FWD, gemm_ffn_in_fwd)
-          RG_F32(R_FFN_OUT_FWD, gemm_ffn_out_fwd) RG_F32(R_QKV_DX, gemm_qkv_dx) RG_F32(R_O_DX, gemm_o_dx)
-          RG_F32(R_FFN_IN_DX, gemm_ffn_in_dx) RG_F32(R_FFN_OUT_DX, gemm_ffn_out_dx)
+        // one kernel per role, chosen at compile time (only R's kernel is instantiated)
+#define RG_F32(ROLE, NAME) if constexpr (R == ROLE) RG_LAUNCH((NAME##_f32<E>), grid, block, 0, s, a); else
+        RG_F32(R_QKV_FWD, gemm_qkv_fwd) RG_F32(R_O_FWD, gemm_o_fwd) RG_F32(R_FFN_IN_FWD, gemm_ffn_in_fwd)
+        RG_F32(R_FFN_OUT_FWD, gemm_ffn_out_fwd) RG_F32(R_QKV_DX, gemm_qkv_dx) RG_F32(R_O_DX, gemm_o_dx)
+        RG_F32(R_FFN_IN_DX, gemm_ffn_in_dx) RG_F32(R_FFN_OUT_DX, gemm_ffn_out_dx)
+        return hipErrorInvalidValue;
 #undef RG_F32
-          default: return hipErrorInvalidValue;
-        }
         return hipGetLastError();
       }
     }
 #define RG_TILES(BM, BN) dim3(((a.N + BN - 1) / BN) * ((a.M + BM - 1) / BM))
-#define RG_LAUNCH_CFG(NAME)                                                                                  \
-  switch (cfg) {                                                                                         \
-    case C_P128x192:                                                                                     \
-      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
-        RG_LAUNCH((NAME##_pipe<128, 192, 2, 2, 2, E>), RG_TILES(128, 192), block, 0, s, a);     \
-      break;                                                                                             \
-    case C_P128x96:                                                                                      \
-      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
-        RG_LAUNCH((NAME##_pipe<128, 96, 4, 1, 3, E>), RG_TILES(128, 96), block, 0, s, a);       \
-      break;                                                                                             \
-    case C_P128x128_2:                                                                                   \
-      RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 2, E>), RG_TILES(128, 128), block, 0, s, a);       \
-      break;                                                                                             \
-    case C_P128x128_3:                                                                                   \
-      RG_LAUNCH((NAME##_pipe<128, 128, 2, 2, 3, E>), RG_TILES(128, 128), block, 0, s, a);       \
-      break;                                                                                             \
-    case C_P256x192_8W:                                                                                  \
-      if constexpr (E != Epi::SwiGlu && E != Epi::Rope)                                                  \
-        RG_LAUNCH((NAME##_pipe8<256, 192, 4, 2, 2, E>), RG_TILES(256, 192), dim3(512), 0, s, a);          \
-      break;                                                                                             \
-    case C_P256x128_8W:                                                                                  \
-      RG_LAUNCH((NAME##_pipe8<256, 128, 4, 2, 3, E>), RG_TILES(256, 128), dim3(512), 0, s, a);            \
-      break;                                                                                             \
-    case C_REG_128x128:                                                                                  \
-      if constexpr (E != Epi::Rope)                                                                      \
-        RG_LAUNCH((NAME<128, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 127) / 128), block, 0, \
-                           s, a);                                                                        \
-      break;                                                                                             \
-    case C_REG_64x128:                                                                                   \
-      if constexpr (E != Epi::Rope)                                                                      \
-        RG_LAUNCH((NAME<64, 128, 2, 2, E>), dim3((a.N + 127) / 128, (a.M + 63) / 64), block, 0,   \
-                           s, a);                                                                        \
-      break;                                                                                             \
+#define RG_CASE(C, K, BM_, BN_, THREADS)                                                    \
+    case C:                                                                                \
+      if constexpr (cfg_has(R, E, C)) RG_LAUNCH((K), RG_TILES(BM_, BN_), dim3(THREADS), 0, s, a); \
+      else return hipErrorInvalidValue;                                                    \
+      break;
+#define RG_LAUNCH_CFG(NAME)                                                               \
+  switch (cfg) {                                                                          \
+    RG_CASE(C_P128x192, (NAME##_pipe<128, 192, 2, 2, 2, E>), 128, 192, 256)               \
+    RG_CASE(C_P128x96, (NAME##_pipe<128, 96, 4, 1, 3, E>), 128, 96, 256)                  \
+    RG_CASE(C_P128x128_2, (NAME##_pipe<128, 128, 2, 2, 2, E>), 128, 128, 256)             \
+    RG_CASE(C_P128x128_3, (NAME##_pipe<128, 128, 2, 2, 3, E>), 128, 128, 256)             \
+    RG_CASE(C_P256x192_8W, (NAME##_pipe8<256, 192, 4, 2, 2, E>), 256, 192, 512)           \
+    RG_CASE(C_P256x128_8W, (NAME##_pipe8<256, 128, 4, 2, 3, E>), 256, 128, 512)           \
+    default: return hipErrorInvalidValue;                                                 \
   }
-    switch (R) {
-      case R_QKV_FWD: RG_LAUNCH_CFG(gemm_qkv_fwd) break;
-      case R_O_FWD: RG_LAUNCH_CFG(gemm_o_fwd) break;
-      case R_FFN_IN_FWD: RG_LAUNCH_CFG(gemm_ffn_in_fwd) break;
-      case R_FFN_OUT_FWD: RG_LAUNCH_CFG(gemm_ffn_out_fwd) break;
-      case R_QKV_DX: RG_LAUNCH_CFG(gemm_qkv_dx) break;
-      case R_O_DX: RG_LAUNCH_CFG(gemm_o_dx) break;
-      case R_FFN_IN_DX: RG_LAUNCH_CFG(gemm_ffn_in_dx) break;
-      case R_FFN_OUT_DX: RG_LAUNCH_CFG(gemm_ffn_out_dx) break;
-      default: return hipErrorInvalidValue;
-    }
+    // only R's kernels are instantiated
+    if constexpr (R == R_QKV_FWD) { RG_LAUNCH_CFG(gemm_qkv_fwd) }
+    else if constexpr (R == R_O_FWD) { RG_LAUNCH_CFG(gemm_o_fwd) }
+    else if constexpr (R == R_FFN_IN_FWD) { RG_LAUNCH_CFG(gemm_ffn_in_fwd) }
+    else if constexpr (R == R_FFN_OUT_FWD) { RG_LAUNCH_CFG(gemm_ffn_out_fwd) }
+    else if constexpr (R == R_QKV_DX) { RG_LAUNCH_CFG(gemm_qkv_dx) }
+    else if constexpr (R == R_O_DX) { RG_LAUNCH_CFG(gemm_o_dx) }
+    else if constexpr (R == R_FFN_IN_DX) { RG_LAUNCH_CFG(gemm_ffn_in_dx) }
+    else if constexpr (R == R_FFN_OUT_DX) { RG_LAUNCH_CFG(gemm_ffn_out_dx) }
+    else return hipErrorInvalidValue;
 #undef RG_LAUNCH_CFG
+#undef RG_CASE
 #undef RG_TILES
     return hipGetLastError();
     }
@@ -897,7 +742,7 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     return hipErrorInvalidValue;
   if ((epi == Epi::SwiGlu || epi == Epi::DSwiGlu) && (a.half % 4)) return hipErrorInvalidValue;
   if (a.out2 && a.ldo2 % 4) return hipErrorInvalidValue;
-  Cfg cfg = C_REG_128x128;
+  Cfg cfg = C_P128x128_3;  // (the fp32 kernel has one tile shape)
   if (dtype == DT_BF16) {
     // 16-B operand chunks and 8-B epilogue vectors
     if (a.K % 8 || a.lda % 8 || a.ldb % 8 || !al16(a.A) || !al16(a.B) || !al8(a.out))
@@ -913,19 +758,16 @@ hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStre
     auto tiles = [&](int bm, int bn) { return (long)((a.M + bm - 1) / bm) * ((a.N + bn - 1) / bn); };
     // two stages (two workgroups per CU) once there are two 128x128 tiles per CU
     const Cfg c128 = tiles(128, 128) >= 512 ? C_P128x128_2 : C_P128x128_3;
-    if (a.K % 64 == 0 && al_epi && small_off) {
-      // the gated and rotary epilogues take only the 64-wide wave tiles
-      const bool glu = epi == Epi::SwiGlu || epi == Epi::DSwiGlu || rope;
-      if (!glu && a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
-      else if (!glu && a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
-      else if (!glu && a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
-      else if (a.K > 1024 && a.N % 128 == 0 && tiles(256, 128) >= 256) cfg = C_P256x128_8W;
-      else cfg = c128;
-    } else {
-      if (rope) return hipErrorInvalidValue;
-      const long tiles128 = (long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-      cfg = tiles128 >= 512 ? C_REG_128x128 : C_REG_64x128;
-    }
+    // (a bf16 stage always meets these: d a multiple of 256, the FFN width of
+    // 64, 16-B aligned buffers, tensors under 2^31 elements)
+    if (a.K % 64 || !al_epi || !small_off) return hipErrorInvalidValue;
+    // the gated and rotary epilogues take only the 64-wide wave tiles
+    const bool glu = epi == Epi::SwiGlu || epi == Epi::DSwiGlu || rope;
+    if (!glu && a.N % 192 == 0 && a.K <= 1024 && tiles(128, 192) >= 256) cfg = C_P128x192;
+    else if (!glu && a.N % 96 == 0 && a.N <= 1024) cfg = C_P128x96;
+    else if (!glu && a.K > 1024 && a.N % 192 == 0 && tiles(256, 192) >= 256) cfg = C_P256x192_8W;
+    else if (a.K > 1024 && a.N % 128 == 0 && tiles(256, 128) >= 256) cfg = C_P256x128_8W;
+    else cfg = c128;
   } else if (dtype == DT_F32) {
     if (!al16(a.out)) return hipErrorInvalidValue;
   } else {

@@ -22,41 +22,6 @@ __device__ float blk_sum(float v, float* red) {
   return t;
 }
 
-// ---------------------------------------------------------------- RMSNorm (one workgroup per row)
-template <typename T>
-__global__ __launch_bounds__(256) void rms_fwd_k(int d, float eps, const T* x, const T* g, T* out,
-                                                  T* xhat, float* rstd) {
-  __shared__ float red[4];
-  const long row = (long)blockIdx.x * d;
-  float ss = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    const float v = St<T>::ld(x, row + i);
-    ss += v * v;
-  }
-  const float rs = rsqrtf(blk_sum<T>(ss, red) / d + eps);
-  if (rstd && threadIdx.x == 0) rstd[blockIdx.x] = rs;
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    const float xh = St<T>::ld(x, row + i) * rs;
-    St<T>::st(out, row + i, xh * St<T>::ld(g, i));
-    if (xhat) St<T>::st(xhat, row + i, xh);
-  }
-}
-
-template <typename T>
-__global__ __launch_bounds__(256) void rms_bwd_k(int d, const T* dn, const T* dres, const T* xhat,
-                                                  const float* rstd, const T* g, T* dx) {
-  __shared__ float red[4];
-  const long row = (long)blockIdx.x * d;
-  float s = 0.f;
-  for (int i = threadIdx.x; i < d; i += blockDim.x)
-    s += St<T>::ld(dn, row + i) * St<T>::ld(g, i) * St<T>::ld(xhat, row + i);
-  const float m2 = blk_sum<T>(s, red) / d, rs = rstd[blockIdx.x];
-  for (int i = threadIdx.x; i < d; i += blockDim.x) {
-    const float gg = St<T>::ld(dn, row + i) * St<T>::ld(g, i);
-    St<T>::st(dx, row + i, St<T>::ld(dres, row + i) + rs * (gg - St<T>::ld(xhat, row + i) * m2));
-  }
-}
-
 // ---------------------------------------------------------------- row norms, bf16, vectorised
 // One 256-thread workgroup per row, eight features per 16-B access (d <= 4096,
 // so at most two per thread).
@@ -226,34 +191,26 @@ hipError_t launch_norm_rows_bwd(int T, int d, Norm norm, const void* gin, const 
 
 hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g, void* out,
                           void* xhat, float* rstd, hipStream_t s) {
+  // bf16 only (the pre-RMS block has no fp32 stage); every bf16 width (d a
+  // multiple of 256 up to 4096) and the stage's 16-B aligned buffers take the
+  // vectorised row kernel
   if (T < 0 || d <= 0 || !x || !g || !out) return hipErrorInvalidValue;
+  if (dtype != DT_BF16 || d % 8 || d > 256 * 8 * NORM_NPT || !al16p(x) || !al16p(g) || !al16p(out) ||
+      (xhat && !al16p(xhat)))
+    return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
-  if (dtype == DT_BF16 && d % 8 == 0 && d <= 256 * 8 * NORM_NPT && al16p(x) && al16p(g) && al16p(out) &&
-      (!xhat || al16p(xhat)))
-    return launch_norm_rows_fwd(T, d, eps, Norm::RMS, x, nullptr, g, nullptr, nullptr, out, xhat, rstd, s);
-  if (dtype == DT_BF16)
-    RG_LAUNCH(rms_fwd_k<bf16>, dim3(T), dim3(256), 0, s, d, eps, (const bf16*)x,
-                       (const bf16*)g, (bf16*)out, (bf16*)xhat, rstd);
-  else
-    RG_LAUNCH(rms_fwd_k<float>, dim3(T), dim3(256), 0, s, d, eps, (const float*)x,
-                       (const float*)g, (float*)out, (float*)xhat, rstd);
-  return hipGetLastError();
+  return launch_norm_rows_fwd(T, d, eps, Norm::RMS, x, nullptr, g, nullptr, nullptr, out, xhat, rstd, s);
 }
 
 hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* dres, const void* xhat,
                           const float* rstd, const void* g, void* dx, hipStream_t s) {
+  // bf16 only, as the forward
   if (T < 0 || d <= 0 || !dn || !dres || !xhat || !rstd || !g || !dx) return hipErrorInvalidValue;
+  if (dtype != DT_BF16 || d % 8 || d > 256 * 8 * NORM_NPT || !al16p(dn) || !al16p(dres) || !al16p(xhat) ||
+      !al16p(g) || !al16p(dx))
+    return hipErrorInvalidValue;
   if (T == 0) return hipSuccess;
-  if (dtype == DT_BF16 && d % 8 == 0 && d <= 256 * 8 * NORM_NPT && al16p(dn) && al16p(dres) && al16p(xhat) &&
-      al16p(g) && al16p(dx))
-    return launch_norm_rows_bwd(T, d, Norm::RMS, dn, xhat, rstd, g, dres, dx, s);
-  if (dtype == DT_BF16)
-    RG_LAUNCH(rms_bwd_k<bf16>, dim3(T), dim3(256), 0, s, d, (const bf16*)dn,
-                       (const bf16*)dres, (const bf16*)xhat, rstd, (const bf16*)g, (bf16*)dx);
-  else
-    RG_LAUNCH(rms_bwd_k<float>, dim3(T), dim3(256), 0, s, d, (const float*)dn,
-                       (const float*)dres, (const float*)xhat, rstd, (const float*)g, (float*)dx);
-  return hipGetLastError();
+  return launch_norm_rows_bwd(T, d, Norm::RMS, dn, xhat, rstd, g, dres, dx, s);
 }
 
 // ---------------------------------------------------------------- layouts
@@ -288,8 +245,6 @@ hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int row
   const dim3 grid((cols + 31) / 32, (rows + 31) / 32), block(256);
   if (in_dtype == DT_F32 && out_dtype == DT_F32)
     RG_LAUNCH((transpose_k<float, float>), grid, block, 0, s, (const float*)in, rows, cols, (float*)out, perm_dh);
-  else if (in_dtype == DT_F32 && out_dtype == DT_BF16)
-    RG_LAUNCH((transpose_k<float, bf16>), grid, block, 0, s, (const float*)in, rows, cols, (bf16*)out, perm_dh);
   else if (in_dtype == DT_BF16 && out_dtype == DT_BF16)
     RG_LAUNCH((transpose_k<bf16, bf16>), grid, block, 0, s, (const bf16*)in, rows, cols, (bf16*)out, perm_dh);
   else
@@ -311,8 +266,8 @@ __global__ __launch_bounds__(256) void pack_swiglu_k(const T* wgu, int d, int F,
 hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s) {
   if (!w_gu || !out || d <= 0 || F <= 0 || F % 32) return hipErrorInvalidValue;
   const dim3 grid(4096), block(256);
-  if (dtype == DT_BF16) RG_LAUNCH(pack_swiglu_k<bf16>, grid, block, 0, s, (const bf16*)w_gu, d, F, (bf16*)out);
-  else RG_LAUNCH(pack_swiglu_k<float>, grid, block, 0, s, (const float*)w_gu, d, F, (float*)out);
+  if (dtype != DT_BF16) return hipErrorInvalidValue;  // the SwiGLU block has no fp32 stage
+  RG_LAUNCH(pack_swiglu_k<bf16>, grid, block, 0, s, (const bf16*)w_gu, d, F, (bf16*)out);
   return hipGetLastError();
 }
 

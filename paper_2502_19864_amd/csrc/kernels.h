@@ -176,7 +176,8 @@ hipError_t launch_adapter_dw_batch(int dtype, const AdapterDwArgs* a, int n, flo
                                    hipStream_t s);
 
 // ---------------------------------------------------------------- row kernels
-// out = RMSNorm(x) * g, xhat/rstd stashes optional
+// out = RMSNorm(x) * g, xhat/rstd stashes optional; bf16 rows (the
+// vectorised row kernel: d % 8 == 0, d <= 4096, 16-B aligned), else refused
 hipError_t launch_rms_fwd(int dtype, int T, int d, float eps, const void* x, const void* g,
                           void* out, void* xhat, float* rstd, hipStream_t s);
 // bf16 rows, d % 8 == 0, d <= 4096, 16-B aligned rows: h = x1 (+ x2);
@@ -189,19 +190,20 @@ hipError_t launch_norm_rows_fwd(int T, int d, float eps, Norm norm, const void* 
 // dz = [dres +] rstd (gamma gin - [mean(gamma gin)] - xhat mean(gamma gin xhat)), LN or RMS
 hipError_t launch_norm_rows_bwd(int T, int d, Norm norm, const void* gin, const void* xhat, const float* rstd,
                                 const void* gamma, const void* dres, void* dz, hipStream_t s);
-// dx = dres + RMSNorm'(dn)
+// dx = dres + RMSNorm'(dn); bf16 rows as launch_rms_fwd
 hipError_t launch_rms_bwd(int dtype, int T, int d, const void* dn, const void* dres,
                           const void* xhat, const float* rstd, const void* g, void* dx,
                           hipStream_t s);
 
 // ---------------------------------------------------------------- parameters
-// out[c, r] = in[r, c] (rows x cols), converting float -> stage dtype; with
+// out[c, r] = in[r, c] (rows x cols), both fp32 or both bf16; with
 // perm_dh > 0 the columns of a [Q | K | V] block (cols = 3 d) come out in
 // per-head order: column p d + h perm_dh + i becomes row (3 h + p) perm_dh + i
 hipError_t launch_transpose(int in_dtype, int out_dtype, const void* in, int rows, int cols,
                             void* out, hipStream_t s, int perm_dh = 0);
 // pack W_gu [d, 2F] into B rows for the SwiGlu epilogue: row p of the result
-// (2F x d) is gate column (p/64)*32 + p%32 if p%64 < 32, else the matching up column
+// (2F x d) is gate column (p/64)*32 + p%32 if p%64 < 32, else the matching up column;
+// bf16 only
 hipError_t launch_pack_swiglu(int dtype, const void* w_gu, int d, int F, void* out, hipStream_t s);
 
 struct AdapterSlot {  // one adapter for the update kernel
