@@ -21,12 +21,12 @@ import numpy as np
 import pytest
 
 from bf16_floor import rel_err_parts, stage_floor, sum_grads
+from gpu_run import run_gpu
 from helpers import TOL, Checker, oracle_run
 import oracle as O
 from paper_2502_19864_amd import binding as B
 from paper_2502_19864_amd.stage import Stage
 from paper_2502_19864_amd.workloads import Workload, make_inputs
-from test_gpu_parity import run_gpu
 
 pytestmark = pytest.mark.gpu
 
