@@ -266,7 +266,8 @@ ringada_status ringada_loss_mse(void* stream, int32_t dtype, const void* y,
  * labels [batch] int32 in [0, n_classes); the fp32 gradients g_wh, g_bh and
  * the mean loss (one device float, may be NULL) are ADDED into: zero them
  * before the first call of an accumulation.  n_classes <= 16; d a multiple of
- * 8; y, dy and w_h 16-B aligned. */
+ * 8; y, dy and w_h 16-B aligned.  Every sum runs over the samples in a fixed
+ * order: the same inputs give the same bits. */
 ringada_status ringada_head_ce(void* stream, int32_t dtype, const void* y,
                                int32_t batch, int32_t seq, int32_t d,
                                const float* w_h, const float* b_h,

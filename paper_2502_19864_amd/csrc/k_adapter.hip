@@ -8,7 +8,8 @@
 // features of one token; row statistics of the norm reduce over the four
 // lanes sharing a token (shuffles) and then over waves (LDS).
 // Weight gradients are long-K (K = tokens), tiny-output contractions: a
-// split-K MFMA kernel with LDS-transposed tiles and fp32 atomics.
+// split-K MFMA kernel with LDS-transposed tiles whose per-chunk partial sums
+// a second kernel adds in chunk order (no atomics: the same bits every run).
 #include <initializer_list>
 
 #include "common.h"

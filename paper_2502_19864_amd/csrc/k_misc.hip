@@ -366,136 +366,143 @@ hipError_t launch_mse(int dtype, const void* y, const void* t, long n, void* dy,
   return hipGetLastError();
 }
 
-// Initiator's classification head on the [CLS] (position 0) token of each
-// sample: logits = y[b, 0, :] W_h + b_h, mean cross-entropy over the batch,
-// dy[b, 0, :] = dlogits W_h^T and zero at every other position, and the head
-// gradients and the loss accumulated into gwh / gbh / loss.
-constexpr int HEAD_C = 16;   // maximum number of classes
-constexpr int HEAD_SPW = 4;  // samples per workgroup (one wave each)
-// Workgroups 0 .. ceil(B / HEAD_SPW) - 1: one wave per sample for the logits,
-// the softmax and the loss, then one thread per feature for the sample's dY
-// row and its share of the W_h gradient (fp32 atomics: the gradients and the
-// loss are sums over the batch, added into the caller's buffers).  The other
-// workgroups zero rows 1..S-1 of every sequence with 16-B stores.
+// Initiator head (Alg. 1: the initiator computes the loss and updates the
+// head): a linear layer on position 0 of each sequence, softmax
+// cross-entropy, mean over the batch.  dy[b, 0, :] = dlogits W_h^T, zero at
+// every other position; the head gradients and the loss are added into
+// gwh / gbh / loss.
+// Workgroup 0 does every sum, so that each result is one thread's sum over
+// the samples in order: the same inputs give the same bits (atomic adds in
+// arrival order would not).  Samples go in chunks of HEAD_CHUNK: one wave
+// per sample for the logits, the softmax and the loss (into LDS), then one
+// thread per feature (in blocks of HEAD_NT features) for the dY rows and the
+// W_h gradient, thread c for the bias gradient of class c and thread 0 for
+// the loss.  The other workgroups
+// zero rows 1..S-1 of every sequence with 16-B stores.
+constexpr int HEAD_C = 16;        // maximum number of classes
+constexpr int HEAD_NT = 1024;     // threads per workgroup (16 waves)
+constexpr int HEAD_CHUNK = 256;   // samples per pass of workgroup 0
 template <typename T, int CN>  // CN: class count bound, compile time (the loops over classes unroll)
-__global__ __launch_bounds__(256) void head_ce_k(const T* y, int B, int S, int d, const float* wh, const float* bh,
-                                                 int C_, const int* labels, T* dy, float* gwh, float* gbh,
-                                                 float* loss) {
+__global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, int d, const float* wh,
+                                                     const float* bh, int C_, const int* labels, T* dy, float* gwh,
+                                                     float* gbh, float* loss) {
   // the two-class instantiation runs only with C == 2: a compile-time class count leaves
-  // no class guard around a load, so the loads of a row go out together instead of one
-  // after the other
+  // no class guard around a load, so the loads of a row go out together
   const int C = CN == 2 ? 2 : C_;
-  const int nce = (B + HEAD_SPW - 1) / HEAD_SPW;
-  if ((int)blockIdx.x >= nce) {
-    const int nz = gridDim.x - nce, z = blockIdx.x - nce;
+  if (blockIdx.x > 0) {
+    const int nz = gridDim.x - 1, z = blockIdx.x - 1;
     const int vpr = d * (int)sizeof(T) / 16;  // 16-B vectors per row
     const long nvec = (long)B * (S - 1) * vpr;
-    for (long v = (long)z * 256 + threadIdx.x; v < nvec; v += (long)nz * 256) {
+    for (long v = (long)z * HEAD_NT + threadIdx.x; v < nvec; v += (long)nz * HEAD_NT) {
       const long rr = v / vpr;
       const long r = (rr / (S - 1)) * S + 1 + rr % (S - 1);
       reinterpret_cast<uint4*>(dy + r * d)[v % vpr] = make_uint4(0, 0, 0, 0);
     }
     return;
   }
-  static_assert(HEAD_SPW * 64 == 256, "one wave per sample of the workgroup");
-  __shared__ float sdl[HEAD_SPW][CN];
-  __shared__ float sloss[HEAD_SPW];
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int j0 = blockIdx.x * HEAD_SPW, j = j0 + wave;
-  if (j < B) {
-    // label and bias first, then the row in 8-feature chunks (16-B loads of y,
-    // 8 x C floats of W_h per chunk): few memory round trips in flight at once
-    const int lab = labels[j];
-    float bias[CN];
+  constexpr int NW = HEAD_NT / 64;
+  __shared__ float sdl[HEAD_CHUNK][CN];
+  __shared__ float sls[HEAD_CHUNK];
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t = threadIdx.x;
+  float bias[CN];
 #pragma unroll
-    for (int c = 0; c < CN; ++c) bias[c] = c < C ? bh[c] : 0.f;
-    const T* yr = y + (long)j * S * d;
-    float lg[CN];
+  for (int c = 0; c < CN; ++c) bias[c] = c < C ? bh[c] : 0.f;
+  // logits, softmax and loss of samples b0 .. b0+nb-1 into sdl / sls, one wave each
+  auto logits = [&](int b0, int nb) {
+    for (int sm = wave; sm < nb; sm += NW) {
+      const int j = b0 + sm, lab = labels[j];
+      const T* yr = y + (long)j * S * d;
+      float lg[CN];
 #pragma unroll
-    for (int c = 0; c < CN; ++c) lg[c] = 0.f;
+      for (int c = 0; c < CN; ++c) lg[c] = 0.f;
 #pragma unroll 2
-    for (int v = lane; v < d / 8; v += 64) {
-      float yv[8];
-      if constexpr (std::is_same_v<T, bf16>) {
-        unpack_frag(ld_frag(yr + 8 * v), yv);
-      } else {
-        const float4 a = reinterpret_cast<const float4*>(yr)[2 * v], b = reinterpret_cast<const float4*>(yr)[2 * v + 1];
-        yv[0] = a.x; yv[1] = a.y; yv[2] = a.z; yv[3] = a.w; yv[4] = b.x; yv[5] = b.y; yv[6] = b.z; yv[7] = b.w;
+      for (int v = lane; v < d / 8; v += 64) {
+        float yv[8];
+        if constexpr (std::is_same_v<T, bf16>) {
+          unpack_frag(ld_frag(yr + 8 * v), yv);
+        } else {
+          const float4 q0 = reinterpret_cast<const float4*>(yr)[2 * v];
+          const float4 q1 = reinterpret_cast<const float4*>(yr)[2 * v + 1];
+          yv[0] = q0.x; yv[1] = q0.y; yv[2] = q0.z; yv[3] = q0.w; yv[4] = q1.x; yv[5] = q1.y; yv[6] = q1.z; yv[7] = q1.w;
+        }
+        const float* wr = wh + (long)8 * v * C;
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+          for (int c = 0; c < CN; ++c)
+            if (c < C) lg[c] += yv[e] * wr[e * C + c];
       }
-      const float* wr = wh + (long)8 * v * C;
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-#pragma unroll
-        for (int c = 0; c < CN; ++c)
-          if (c < C) lg[c] += yv[e] * wr[e * C + c];
-    }
-    float mx = -INFINITY;
-#pragma unroll
-    for (int c = 0; c < CN; ++c)
-      if (c < C) {
-        lg[c] = wave_sum(lg[c]) + bias[c];
-        mx = fmaxf(mx, lg[c]);
-      }
-    float se = 0.f, ll = 0.f;
-#pragma unroll
-    for (int c = 0; c < CN; ++c)
-      if (c < C) {
-        se += __expf(lg[c] - mx);
-        if (c == lab) ll = lg[c];
-      }
-    if (lane == 0) {
-      sloss[wave] = -(ll - mx - __logf(se)) / (float)B;
-#pragma unroll
-      for (int c = 0; c < CN; ++c)
-        sdl[wave][c] = c < C ? (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B : 0.f;
-    }
-  } else if (lane < CN) {
-    sdl[wave][lane] = 0.f;
-    if (lane == 0) sloss[wave] = 0.f;
-  }
-  __syncthreads();
-  // the workgroup's samples summed first: one atomic add per address per
-  // workgroup (adds to one address are serialised in memory)
-  if (threadIdx.x <= CN) {
-    const int c = threadIdx.x;
-    float t = 0.f;
-#pragma unroll
-    for (int w = 0; w < HEAD_SPW; ++w) t += c == CN ? sloss[w] : sdl[w][c];
-    if (c == CN) {
-      if (loss) unsafeAtomicAdd(loss, t);
-    } else if (c < C) {
-      unsafeAtomicAdd(gbh + c, t);
-    }
-  }
-  const int ns = min(HEAD_SPW, B - j0);
-  for (int i = threadIdx.x; i < d; i += 256) {
-    float w[CN], acc[CN], yi[HEAD_SPW];
-#pragma unroll
-    for (int c = 0; c < CN; ++c) {
-      w[c] = c < C ? wh[(long)i * C + c] : 0.f;
-      acc[c] = 0.f;
-    }
-#pragma unroll
-    for (int s = 0; s < HEAD_SPW; ++s) {  // unconditional load (sample clamped), masked after
-      const float v = St<T>::ld(y, (long)(j0 + min(s, ns - 1)) * S * d + i);
-      yi[s] = s < ns ? v : 0.f;
-    }
-#pragma unroll
-    for (int s = 0; s < HEAD_SPW; ++s) {
-      if (s >= ns) break;
-      float g = 0.f;
+      float mx = -INFINITY;
 #pragma unroll
       for (int c = 0; c < CN; ++c)
         if (c < C) {
-          acc[c] += yi[s] * sdl[s][c];
-          g += sdl[s][c] * w[c];
+          lg[c] = wave_sum(lg[c]) + bias[c];
+          mx = fmaxf(mx, lg[c]);
         }
-      St<T>::st(dy, (long)(j0 + s) * S * d + i, g);
-    }
+      float se = 0.f, ll = 0.f;
 #pragma unroll
-    for (int c = 0; c < CN; ++c)
-      if (c < C) unsafeAtomicAdd(gwh + (long)i * C + c, acc[c]);
+      for (int c = 0; c < CN; ++c)
+        if (c < C) {
+          se += __expf(lg[c] - mx);
+          if (c == lab) ll = lg[c];
+        }
+      if (lane == 0) {
+        sls[sm] = -(ll - mx - __logf(se)) / (float)B;
+#pragma unroll
+        for (int c = 0; c < CN; ++c)
+          sdl[sm][c] = c < C ? (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B : 0.f;
+      }
+    }
+  };
+  // A batch of at most HEAD_CHUNK samples has its logits formed once; larger
+  // batches re-form each chunk's for every block of HEAD_NT features.
+  const bool one_chunk = B <= HEAD_CHUNK;
+  float bacc = 0.f, lacc = 0.f;
+  for (int fb = 0; fb * HEAD_NT < d; ++fb) {
+    const int i = t + fb * HEAD_NT;
+    const bool iv = i < d;
+    float wv[CN], gacc[CN];
+#pragma unroll
+    for (int c = 0; c < CN; ++c) {
+      wv[c] = (iv && c < C) ? wh[(long)i * C + c] : 0.f;
+      gacc[c] = 0.f;
+    }
+    for (int b0 = 0; b0 < B; b0 += HEAD_CHUNK) {
+      const int nb = min(HEAD_CHUNK, B - b0);
+      if (fb == 0 || !one_chunk) {  // the same for every thread
+        logits(b0, nb);
+        __syncthreads();
+      }
+      // dY row and the W_h gradient of feature i (thread = feature), the samples in order
+      if (iv)
+        for (int sm = 0; sm < nb; ++sm) {
+          const long row = (long)(b0 + sm) * S * d;
+          const float yi = St<T>::ld(y, row + i);
+          float g = 0.f;
+#pragma unroll
+          for (int c = 0; c < CN; ++c)
+            if (c < C) {
+              gacc[c] += yi * sdl[sm][c];
+              g += sdl[sm][c] * wv[c];
+            }
+          St<T>::st(dy, row + i, g);
+        }
+      if (fb == 0) {  // the bias gradient and the loss, once
+        if (t < C)
+          for (int sm = 0; sm < nb; ++sm) bacc += sdl[sm][t];
+        if (t == 0)
+          for (int sm = 0; sm < nb; ++sm) lacc += sls[sm];
+      }
+      if (!one_chunk) __syncthreads();  // the next chunk overwrites sdl / sls
+    }
+    if (iv) {
+#pragma unroll
+      for (int c = 0; c < CN; ++c)
+        if (c < C) gwh[(long)i * C + c] += gacc[c];
+    }
   }
+  if (t < C) gbh[t] += bacc;
+  if (t == 0 && loss) *loss += lacc;
 }
 
 hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const float* wh, const float* bh,
@@ -508,10 +515,9 @@ hipError_t launch_head_ce(int dtype, const void* y, int B, int S, int d, const f
   if (d % 8 || (d * es) % 16 ||
       (reinterpret_cast<uintptr_t>(dy) | reinterpret_cast<uintptr_t>(y) | reinterpret_cast<uintptr_t>(wh)) & 15u)
     return hipErrorInvalidValue;
-  const int nce = (B + HEAD_SPW - 1) / HEAD_SPW;
   const long nvec = (long)B * (S - 1) * (long)(d * es / 16);
-  const int nz = (int)std::min<long>(256, (nvec + 255) / 256);
-  const dim3 grid(nce + nz), block(256);
+  const int nz = (int)std::min<long>(255, (nvec + HEAD_NT - 1) / HEAD_NT);
+  const dim3 grid(1 + nz), block(HEAD_NT);
   if (dtype == DT_BF16) {
     if (C == 2)
       RG_LAUNCH((head_ce_k<bf16, 2>), grid, block, 0, s, (const bf16*)y, B, S, d, wh, bh, C, labels, (bf16*)dy,

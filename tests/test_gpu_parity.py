@@ -348,6 +348,52 @@ def test_wide_adapter_parity(torch, name):
         st.close()
 
 
+def test_training_iterations_are_bitwise_reproducible(torch):
+    """Two fresh stages on the same inputs, two Alg. 1 iterations each
+    (forward, [CLS] head loss and head update, backward to the cut-off,
+    adapter update): every adapter weight, the head and the last loss come
+    out bit for bit the same.  No result of the path depends on the order in
+    which workgroups finish (no floating-point atomics anywhere)."""
+    w = Workload("rep_bert", "bert", "bf16", 3, 256, 4, 512, 64, 64, 8, 1, "cls_ce", 2301)
+    inp = make_inputs(w)
+    c, lr = w.lowest_unfrozen, 1e-2
+
+    def train():
+        st = Stage(w, inp)
+        try:
+            x = st.upload(inp["x"])
+            y, dy = st.empty(*inp["x"].shape), st.empty(*inp["x"].shape)
+            nwh = inp["w_h"].size
+            hp = st.f32(np.concatenate([inp["w_h"].ravel(), inp["b_h"].ravel()]))
+            hg = torch.zeros_like(hp)
+            wh, bh, gwh, gbh = hp[:nwh].view(inp["w_h"].shape), hp[nwh:], hg[:nwh].view(inp["w_h"].shape), hg[nwh:]
+            lab = torch.from_numpy(inp["labels"]).to(st.dev)
+            loss = torch.zeros(1, dtype=torch.float32, device=st.dev)
+            for _ in range(2):
+                st.forward(x, y, c)
+                loss.zero_()
+                B.ringada_head_ce(st.sptr, st.desc.dtype, y, w.batch, w.seq, w.d_model, wh, bh, 2, lab, dy, gwh, gbh,
+                                  loss)
+                B.ringada_sgd_f32(st.sptr, hp, hg, hp.numel(), lr)
+                st.backward(dy, c)
+                st.step(c, lr)
+            torch.cuda.synchronize()
+            out = [hp.cpu().numpy(), loss.cpu().numpy(), y.float().cpu().numpy()]
+            for pair in st.adapters:
+                for t in pair:
+                    out += [t["w_down"].cpu().numpy(), t["w_up"].cpu().numpy()]
+            return out
+        finally:
+            st.close()
+
+    first, second = train(), train()
+    assert len(first) == len(second)
+    for k, (a_, b_) in enumerate(zip(first, second)):
+        assert np.array_equal(a_, b_), f"result {k} differs between two identical runs"
+    # the updates did something: the trained adapters differ from their start
+    assert not np.array_equal(first[3 + 2 * 2 * c], inp["adapters"][c][0]["w_down"].astype(np.float32))
+
+
 def test_state_machine_and_workspace_errors(torch):
     w = SMALL["small_bert"]
     inp = make_inputs(w)

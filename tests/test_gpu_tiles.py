@@ -103,7 +103,7 @@ def test_tile_configuration_parity(torch, name):
 
 
 # ---------------------------------------------------------------- loss helpers
-def _head_case(torch, dtype, n_classes, batch=6, seq=5, d=256, seed=2201):
+def _head_case(torch, dtype, n_classes, batch=6, seq=5, d=256, seed=2201, repeat=1):
     """ringada_head_ce on seeded inputs against the oracle's head: the loss,
     the head's gradients and the dY rows (position 0 of each sequence; every
     other row must come back zero)."""
@@ -123,9 +123,16 @@ def _head_case(torch, dtype, n_classes, batch=6, seq=5, d=256, seed=2201):
     loss = torch.zeros(1, dtype=torch.float32, device=dev)
     lab = torch.from_numpy(labels).to(dev)
     s = torch.cuda.current_stream(dev).cuda_stream
-    B.ringada_head_ce(s, B.BF16 if dtype == "bf16" else B.F32, yt, batch, seq, d, wht, bht, n_classes, lab, dyt,
-                      gwh, gbh, loss)
-    torch.cuda.synchronize()
+    runs = []
+    for _ in range(repeat):  # fresh accumulators each time: the same bits every call
+        gwh.zero_(); gbh.zero_(); loss.zero_(); dyt.fill_(float("nan"))
+        B.ringada_head_ce(s, B.BF16 if dtype == "bf16" else B.F32, yt, batch, seq, d, wht, bht, n_classes, lab, dyt,
+                          gwh, gbh, loss)
+        torch.cuda.synchronize()
+        runs.append([t_.clone() for t_ in (loss, dyt, gwh, gbh)])
+    for r in runs[1:]:
+        for a_, b_ in zip(runs[0], r):
+            assert torch.equal(a_, b_), "ringada_head_ce gave different bits on the same inputs"
     ref_loss, ref_dy, ref_gwh, ref_gbh = O.cls_head_ce(y.astype(np.float64), wh.astype(np.float64),
                                                        bh.astype(np.float64), labels)
     return (loss.cpu().numpy()[0], dyt.float().cpu().numpy(), gwh.cpu().numpy(), gbh.cpu().numpy(),
@@ -133,19 +140,22 @@ def _head_case(torch, dtype, n_classes, batch=6, seq=5, d=256, seed=2201):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16"])
-@pytest.mark.parametrize("n_classes", [2, 5, 16])
-def test_head_ce_classes(torch, dtype, n_classes):
+@pytest.mark.parametrize("n_classes,batch,d", [(2, 6, 256), (5, 6, 256), (16, 6, 256), (5, 300, 2048)])
+def test_head_ce_classes(torch, dtype, n_classes, batch, d):
     """Both instantiations of the head kernel (two classes, and up to 16) in
-    both storage types.  The loss and the head gradients are fp32 sums of
-    exact inputs (bound 1e-4); the bf16 dY is one rounding of an fp32 dot
-    product (bound: two bf16 units in the last place, 2^-7, relative to the
-    tensor's largest value)."""
-    loss, dy, gwh, gbh, rloss, rdy, rgwh, rgbh = _head_case(torch, dtype, n_classes, seed=2201 + n_classes)
-    chk = Checker(f"head_ce {dtype} C={n_classes}", tol=TOL["f32"])
+    both storage types, and a batch of more than one 256-sample chunk with
+    more than one 1024-feature block.  The loss and the head gradients are
+    fp32 sums of exact inputs (bound 1e-4); the bf16 dY is one rounding of an
+    fp32 dot product (bound: two bf16 units in the last place, 2^-7, relative
+    to the tensor's largest value).  Three calls on the same inputs give the
+    same bits."""
+    loss, dy, gwh, gbh, rloss, rdy, rgwh, rgbh = _head_case(torch, dtype, n_classes, batch=batch, d=d,
+                                                            seed=2201 + n_classes + batch, repeat=3)
+    chk = Checker(f"head_ce {dtype} C={n_classes} B={batch} d={d}", tol=TOL["f32"])
     chk("loss", np.array([loss]), np.array([rloss]))
     chk("g_wh", gwh, rgwh)
     chk("g_bh", gbh, rgbh)
-    dchk = Checker(f"head_ce {dtype} C={n_classes}", tol=TOL["f32"] if dtype == "f32" else 2.0 ** -7)
+    dchk = Checker(f"head_ce {dtype} C={n_classes} B={batch} d={d}", tol=TOL["f32"] if dtype == "f32" else 2.0 ** -7)
     dchk("dy", dy, rdy)
     assert np.all(dy[:, 1:] == 0), "dY rows past position 0 must be written as zeros"
     chk.done()
