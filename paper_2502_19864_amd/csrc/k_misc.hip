@@ -404,53 +404,73 @@ __global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, i
   __shared__ float sdl[HEAD_CHUNK][CN];
   __shared__ float sls[HEAD_CHUNK];
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, t = threadIdx.x;
-  float bias[CN];
-#pragma unroll
-  for (int c = 0; c < CN; ++c) bias[c] = c < C ? bh[c] : 0.f;
   // logits, softmax and loss of samples b0 .. b0+nb-1 into sdl / sls, one wave each
+  // samples per wave pass: two for the two-class head, so that both rows'
+  // loads are in flight together (the second clamped); one for up to 16
+  // classes, whose logits take the registers
+  constexpr int PAIR = CN <= 4 ? 2 : 1;
   auto logits = [&](int b0, int nb) {
-    for (int sm = wave; sm < nb; sm += NW) {
-      const int j = b0 + sm, lab = labels[j];
-      const T* yr = y + (long)j * S * d;
-      float lg[CN];
+    for (int sm = wave; sm < nb; sm += PAIR * NW) {
+      int smk[PAIR];
+      const T* yr[PAIR];
 #pragma unroll
-      for (int c = 0; c < CN; ++c) lg[c] = 0.f;
-#pragma unroll 2
+      for (int k = 0; k < PAIR; ++k) {
+        smk[k] = min(sm + k * NW, nb - 1);
+        yr[k] = y + (long)(b0 + smk[k]) * S * d;
+      }
+      float lg[PAIR][CN];
+#pragma unroll
+      for (int k = 0; k < PAIR; ++k)
+#pragma unroll
+        for (int c = 0; c < CN; ++c) lg[k][c] = 0.f;
       for (int v = lane; v < d / 8; v += 64) {
-        float yv[8];
-        if constexpr (std::is_same_v<T, bf16>) {
-          unpack_frag(ld_frag(yr + 8 * v), yv);
-        } else {
-          const float4 q0 = reinterpret_cast<const float4*>(yr)[2 * v];
-          const float4 q1 = reinterpret_cast<const float4*>(yr)[2 * v + 1];
-          yv[0] = q0.x; yv[1] = q0.y; yv[2] = q0.z; yv[3] = q0.w; yv[4] = q1.x; yv[5] = q1.y; yv[6] = q1.z; yv[7] = q1.w;
+        float yv[PAIR][8];
+#pragma unroll
+        for (int k = 0; k < PAIR; ++k) {
+          if constexpr (std::is_same_v<T, bf16>) {
+            unpack_frag(ld_frag(yr[k] + 8 * v), yv[k]);
+          } else {
+            const float4 q0 = reinterpret_cast<const float4*>(yr[k])[2 * v];
+            const float4 q1 = reinterpret_cast<const float4*>(yr[k])[2 * v + 1];
+            yv[k][0] = q0.x; yv[k][1] = q0.y; yv[k][2] = q0.z; yv[k][3] = q0.w;
+            yv[k][4] = q1.x; yv[k][5] = q1.y; yv[k][6] = q1.z; yv[k][7] = q1.w;
+          }
         }
         const float* wr = wh + (long)8 * v * C;
 #pragma unroll
         for (int e = 0; e < 8; ++e)
 #pragma unroll
           for (int c = 0; c < CN; ++c)
-            if (c < C) lg[c] += yv[e] * wr[e * C + c];
+            if (c < C) {
+              const float wc = wr[e * C + c];
+#pragma unroll
+              for (int k = 0; k < PAIR; ++k) lg[k][c] += yv[k][e] * wc;
+            }
       }
-      float mx = -INFINITY;
 #pragma unroll
-      for (int c = 0; c < CN; ++c)
-        if (c < C) {
-          lg[c] = wave_sum(lg[c]) + bias[c];
-          mx = fmaxf(mx, lg[c]);
-        }
-      float se = 0.f, ll = 0.f;
-#pragma unroll
-      for (int c = 0; c < CN; ++c)
-        if (c < C) {
-          se += __expf(lg[c] - mx);
-          if (c == lab) ll = lg[c];
-        }
-      if (lane == 0) {
-        sls[sm] = -(ll - mx - __logf(se)) / (float)B;
+      for (int k = 0; k < PAIR; ++k) {
+        if (sm + k * NW >= nb) break;  // wave-uniform
+        const int lab = labels[b0 + smk[k]];
+        float mx = -INFINITY;
 #pragma unroll
         for (int c = 0; c < CN; ++c)
-          sdl[sm][c] = c < C ? (__expf(lg[c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B : 0.f;
+          if (c < C) {
+            lg[k][c] = wave_sum(lg[k][c]) + bh[c];
+            mx = fmaxf(mx, lg[k][c]);
+          }
+        float se = 0.f, ll = 0.f;
+#pragma unroll
+        for (int c = 0; c < CN; ++c)
+          if (c < C) {
+            se += __expf(lg[k][c] - mx);
+            if (c == lab) ll = lg[k][c];
+          }
+        if (lane == 0) {
+          sls[smk[k]] = -(ll - mx - __logf(se)) / (float)B;
+#pragma unroll
+          for (int c = 0; c < CN; ++c)
+            sdl[smk[k]][c] = c < C ? (__expf(lg[k][c] - mx) / se - (c == lab ? 1.f : 0.f)) / (float)B : 0.f;
+        }
       }
     }
   };
@@ -473,19 +493,27 @@ __global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, i
         logits(b0, nb);
         __syncthreads();
       }
-      // dY row and the W_h gradient of feature i (thread = feature), the samples in order
+      // dY row and the W_h gradient of feature i (thread = feature), the samples in
+      // order; UNR samples' loads in flight at once (clamped, masked after)
+      constexpr int UNR = CN <= 4 ? 8 : 4;
       if (iv)
-        for (int sm = 0; sm < nb; ++sm) {
-          const long row = (long)(b0 + sm) * S * d;
-          const float yi = St<T>::ld(y, row + i);
-          float g = 0.f;
+        for (int sm0 = 0; sm0 < nb; sm0 += UNR) {
+          float yv[UNR];
 #pragma unroll
-          for (int c = 0; c < CN; ++c)
-            if (c < C) {
-              gacc[c] += yi * sdl[sm][c];
-              g += sdl[sm][c] * wv[c];
-            }
-          St<T>::st(dy, row + i, g);
+          for (int u = 0; u < UNR; ++u) yv[u] = St<T>::ld(y, (long)(b0 + min(sm0 + u, nb - 1)) * S * d + i);
+#pragma unroll
+          for (int u = 0; u < UNR; ++u) {
+            const int sm = sm0 + u;
+            if (sm >= nb) break;
+            float g = 0.f;
+#pragma unroll
+            for (int c = 0; c < CN; ++c)
+              if (c < C) {
+                gacc[c] += yv[u] * sdl[sm][c];
+                g += sdl[sm][c] * wv[c];
+              }
+            St<T>::st(dy, (long)(b0 + sm) * S * d + i, g);
+          }
         }
       if (fb == 0) {  // the bias gradient and the loss, once
         if (t < C)
