@@ -92,8 +92,10 @@ typedef struct {
 
 /* Frozen weights of one block, device pointers in the stage dtype, all
  * row-major [in, out].  Pointers marked (post-LN) must be NULL for the pre-RMS
- * arch and non-NULL for the post-LN arch.  The memory is borrowed: it must
- * stay valid and unchanged until ringada_stage_destroy. */
+ * arch and non-NULL for the post-LN arch.  The norm gains and shifts
+ * (norm1_g, norm1_b, norm2_g, norm2_b) must be 16-byte aligned
+ * (ringada_stage_bind_block returns RINGADA_E_INVALID otherwise).  The memory
+ * is borrowed: it must stay valid and unchanged until ringada_stage_destroy. */
 typedef struct {
   const void* w_qkv;   /* [d, 3d]; output columns are [Q | K | V], head h owns
                           columns [h*d_head, (h+1)*d_head) of each */

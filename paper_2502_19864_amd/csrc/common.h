@@ -31,6 +31,9 @@ template <> struct St<float> {
     float4 q = *reinterpret_cast<const float4*>(p + i);
     v[0] = q.x; v[1] = q.y; v[2] = q.z; v[3] = q.w;
   }
+  static __device__ __forceinline__ void st_nt(float* p, long i, float v) {  // streamed (st16 below)
+    __builtin_nontemporal_store(v, p + i);
+  }
   static __device__ __forceinline__ void st4(float* p, long i, const float v[4]) {
     *reinterpret_cast<float4*>(p + i) = make_float4(v[0], v[1], v[2], v[3]);
   }
@@ -38,6 +41,9 @@ template <> struct St<float> {
 template <> struct St<bf16> {
   static __device__ __forceinline__ float ld(const bf16* p, long i) { return bf2f(p[i]); }
   static __device__ __forceinline__ void st(bf16* p, long i, float v) { p[i] = f2bf(v); }
+  static __device__ __forceinline__ void st_nt(bf16* p, long i, float v) {  // streamed (st16 below)
+    __builtin_nontemporal_store(f2bf(v), p + i);
+  }
   // four consecutive elements (8 B aligned)
   static __device__ __forceinline__ void ld4(const bf16* p, long i, float v[4]) {
     uint2 q = *reinterpret_cast<const uint2*>(p + i);
@@ -49,6 +55,18 @@ template <> struct St<bf16> {
     q.x = f2bf2(v[0], v[1]);
     q.y = f2bf2(v[2], v[3]);
     *reinterpret_cast<uint2*>(p + i) = q;
+  }
+  // the same, streamed when nt (st16 and stream_out below)
+  static __device__ __forceinline__ void st4s(bf16* p, long i, const float v[4], bool nt) {
+    const uint32_t lo = f2bf2(v[0], v[1]), hi = f2bf2(v[2], v[3]);
+    typedef unsigned int u32x2_t __attribute__((ext_vector_type(2)));
+    if (nt) {
+      __builtin_nontemporal_store(u32x2_t{lo, hi}, reinterpret_cast<u32x2_t*>(p + i));
+    } else {
+      uint32_t* d = reinterpret_cast<uint32_t*>(p + i);
+      d[0] = lo;
+      d[1] = hi;
+    }
   }
 };
 
@@ -121,6 +139,36 @@ __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
 
 __device__ __forceinline__ bf16x8 ld_frag(const bf16* p) {  // 16 B
   return *reinterpret_cast<const bf16x8*>(p);
+}
+// Output stores with the non-temporal hint.  A plain store leaves the line dirty
+// in this XCD's L2, to be written back when the kernel ends; every kernel's
+// outputs are read by the next kernel from all eight XCDs, so that write-back
+// sits on the kernel's tail.  A streamed line goes out at once, but is not
+// allocated in the Infinity Cache either, so the next kernel reads it from HBM.
+// Measured (write, then read in the next kernel): streaming wins up to 32 MiB
+// per tensor, the eight L2s' capacity, and loses from 64 MiB on, where the
+// plain stores' Infinity Cache hits dominate.  So an output is streamed iff it
+// is at most NT_MAX_BYTES, and every streamed store writes whole 128-B lines
+// per instruction (scattered pieces would leave the L2 unmerged).
+// Given a plain and a non-temporal store of the same value to the same address
+// in the two arms of a branch, the compiler merges them into one store that
+// carries only the attributes both share, which drops the hint.  So the plain
+// arm stores the same bytes in two halves: a different instruction, which the
+// compiler cannot merge with the streamed one (the backend may pair the
+// halves again inside the plain arm).  Small outputs ([T][m] stashes, split-K
+// partials) are always streamed (st_nt).
+constexpr long NT_MAX_BYTES = 32l << 20;
+__device__ __forceinline__ bool stream_out(long bytes) { return bytes <= NT_MAX_BYTES; }
+__device__ __forceinline__ void st16(void* p, bf16x8 v, bool nt) {
+  typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+  const u32x4_t q = __builtin_bit_cast(u32x4_t, v);
+  if (nt) {
+    __builtin_nontemporal_store(q, static_cast<u32x4_t*>(p));
+  } else {
+    uint2* d = static_cast<uint2*>(p);
+    d[0] = make_uint2(q.x, q.y);
+    d[1] = make_uint2(q.z, q.w);
+  }
 }
 __device__ __forceinline__ bf16x8 zero_frag() {
   uint4 z = make_uint4(0, 0, 0, 0);

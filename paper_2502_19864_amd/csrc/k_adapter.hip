@@ -24,14 +24,17 @@ constexpr int GP = MB + 8;
 // ================================================================ bf16 forward, d <= 1024
 // One workgroup of 16 waves per 16 tokens: the whole adapter, the residual
 // add and the norm in one kernel.
-// Laid out so that nothing waits twice on memory and every global row access
-// is contiguous: all global loads (the z
-// tile, the weight fragments of both projections, the residual) are issued
-// before the first barrier; the up projection's fp32 result is staged in LDS;
-// the add + norm phase then runs one wave per token (NW == TOK), so the row
-// statistics are wave reductions and each lane handles features
-// 4*lane + 256*j, which makes every load and store of that phase one
-// contiguous 512-B run per instruction.  The down projection's k-slice
+// Laid out so that nothing waits twice on memory and every global access
+// moves 16 B per lane: all global loads are issued before the first barrier
+// (the norm's gain and shift once per workgroup, the residual and z tiles by
+// DMA into LDS, the weight fragments of both projections into registers); the
+// up projection's fp32 result is staged in LDS; the add + norm phase then
+// runs one wave per token (NW == TOK), so the row statistics are wave
+// reductions, and each lane handles the 8 features of chunks lane + 64 j.
+// The memory pipe of a CU takes about as long per wave instruction whatever
+// its width, so the 16-B accesses (with the gain and shift loaded once, not
+// by every wave) cut this kernel's load and store instructions by a third.
+// The down projection's k-slice
 // partial sums go through LDS unit-major, [slice][unit][token] with a token
 // stride of 17 floats: the MFMA writes (16 tokens of 4 units per lane group)
 // and the GELU phase's reads (one unit per lane) spread over the banks,
@@ -43,15 +46,40 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   constexpr int SLICE = D / KS, NSTEP = SLICE / 32;
   static_assert(NW == TOK, "one wave per token in the norm phase");
   extern __shared__ __attribute__((aligned(16))) unsigned char smem[];
+  constexpr int NC = D / 8, NJ = (NC + 63) / 64;  // 16-B chunks per row; per lane in the norm phase
   bf16* sZ = reinterpret_cast<bf16*>(smem);                // [TOK][DP]
   bf16* sG = sZ + TOK * DP;                                // [TOK][GP]
   float* sUp = reinterpret_cast<float*>(sG + TOK * GP);    // [KS][MB][TOKP]
   float* sV = sUp + KS * MB * TOKP;                        // [TOK][VP]
+  bf16* sR = reinterpret_cast<bf16*>(sV + TOK * VP);       // [TOK][D] residual
+  bf16* sGB = sR + TOK * D;                                // [2][D] gain, shift
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T, t0 = xcd_block(blockIdx.x, gridDim.x) * TOK;
   const bf16* z = static_cast<const bf16*>(a.z);
+  const bool nt = stream_out((long)T * D * 2);  // outputs streamed (common.h)
 
-  // ---- every global load up front.  The z tile goes by DMA straight into its padded LDS
+  // ---- every global load up front, the ones needed last first: the z wait below then
+  // covers them as well.  The norm's gain and shift: 2 NC chunks, one per thread of the
+  // first waves; every wave loads (a chunk index taken modulo), so no load is conditional
+  // and the compiler's wait counts stay exact.  An absent gain / shift reads z's first row.
+  const bf16* gp = static_cast<const bf16*>(a.norm != Norm::None ? a.gamma : a.z);
+  const bf16* bp = static_cast<const bf16*>(a.norm == Norm::LN ? a.beta : a.z);
+  const int gbc = (wave * 64 + lane) % (2 * NC);
+  const uint4 gbv = *reinterpret_cast<const uint4*>(gbc < NC ? gp + 8 * gbc : bp + 8 * (gbc - NC));
+  {  // the residual tile by DMA into unpadded LDS rows: instruction k covers slots
+     // 64 k .. 64 k + 63, slot s = chunk s % NC of row s / NC; 8 FB instructions
+    const bf16* rb = static_cast<const bf16*>(a.res) + (long)t0 * D;
+#pragma unroll
+    for (int i = 0; i < (FB + 1) / 2; ++i) {
+      const int k = i * NW + wave;
+      if (k < 8 * FB) {  // wave-uniform
+        const int sl = k * 64 + lane, r = sl / NC, c = sl % NC;
+        dma16_m0(rb, t0 + r < T ? (uint32_t)((r * D + 8 * c) * 2) : 0u,
+                 lds_addr(sR) + (uint32_t)__builtin_amdgcn_readfirstlane(k * 1024));
+      }
+    }
+  }
+  // The z tile goes by DMA straight into its padded LDS
   // rows: 16-B slot s is chunk s % SPR of row s / SPR, the row's last slot is padding; the
   // slots past the tile land in the sG / sUp space, which is written only after the wait.
   // Slots with no data (padding, rows past T) load the tile's first chunk instead.
@@ -87,25 +115,12 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   const int tw = t0 + wave;  // this wave's token in the norm phase
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
-  // the norm's affine parameters, loaded with everything else rather than after the last
-  // barrier, and the residual row last: it is needed last.  No load here is conditional
-  // (an absent gamma / beta reads z's first row instead, a row past T row 0), so the
-  // compiler's wait counts stay exact and the weight fragments are not waited for along
-  // with the residual.
-  const bf16* gp = static_cast<const bf16*>(a.norm != Norm::None ? a.gamma : a.z);
-  const bf16* bp = static_cast<const bf16*>(a.norm == Norm::LN ? a.beta : a.z);
-  uint2 rr[FB], gmv[FB], btv[FB];
-#pragma unroll
-  for (int j = 0; j < FB; ++j) {
-    const int f = 4 * lane + 256 * j;
-    gmv[j] = *reinterpret_cast<const uint2*>(gp + f);
-    btv[j] = *reinterpret_cast<const uint2*>(bp + f);
-    rr[j] = *reinterpret_cast<const uint2*>(static_cast<const bf16*>(a.res) + wrow + f);
-  }
-  // the z tile has landed once no more than the weight-fragment loads issued after it are
-  // pending (vmcnt counts in issue order)
+  // the z tile (and the residual tile and the gain and shift, issued before it) have
+  // landed once no more than the weight-fragment loads issued after it are pending
+  // (vmcnt counts in issue order)
   if (has_ad) asm volatile("s_waitcnt vmcnt(%0)" ::"n"(NSTEP + 2 * FB) : "memory");
   else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  if (wave * 64 + lane < 2 * NC) *reinterpret_cast<uint4*>(sGB + 8 * gbc) = gbv;
   __syncthreads();
 
   // ---- U^T[unit][token] = W_down^T[unit][:] . z[token][:], k split over KS waves
@@ -122,7 +137,7 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
       float sum = 0.f;
 #pragma unroll
       for (int k2 = 0; k2 < KS; ++k2) sum += sUp[(k2 * MB + unit) * TOKP + tok];
-      if (a.u && t0 + tok < T) static_cast<bf16*>(a.u)[(long)(t0 + tok) * MB + unit] = f2bf(sum);
+      if (a.u && t0 + tok < T) St<bf16>::st_nt(static_cast<bf16*>(a.u), (long)(t0 + tok) * MB + unit, sum);
       sG[tok * GP + unit] = f2bf(gelu_fast(sum));
     }
     __syncthreads();
@@ -141,25 +156,38 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
     __syncthreads();
   }
 
-  // ---- add + norm, wave = token
+  // ---- add + norm, wave = token; lane: the 8 features of chunk lane + 64 j
   if (!twv) return;
-  float v[FB][4];
+  float v[NJ][8];
 #pragma unroll
-  for (int j = 0; j < FB; ++j) {
-    const int f = 4 * lane + 256 * j;
-    const float4 up = has_ad ? *reinterpret_cast<const float4*>(sV + wave * VP + f) : make_float4(0.f, 0.f, 0.f, 0.f);
-    float zz[4];
-    St<bf16>::ld4(sZ, wave * DP + f, zz);
-    const float r4[4] = {__uint_as_float(rr[j].x << 16), __uint_as_float(rr[j].x & 0xffff0000u),
-                         __uint_as_float(rr[j].y << 16), __uint_as_float(rr[j].y & 0xffff0000u)};
-    v[j][0] = up.x + zz[0] + r4[0];
-    v[j][1] = up.y + zz[1] + r4[1];
-    v[j][2] = up.z + zz[2] + r4[2];
-    v[j][3] = up.w + zz[3] + r4[3];
+  for (int j = 0; j < NJ; ++j) {
+    const int c = lane + 64 * j;
+    if (NC % 64 == 0 || c < NC) {
+      float zz[8], r8[8];
+      unpack_frag(*reinterpret_cast<const bf16x8*>(sZ + wave * DP + 8 * c), zz);
+      unpack_frag(*reinterpret_cast<const bf16x8*>(sR + wave * D + 8 * c), r8);
+      float4 u0 = make_float4(0.f, 0.f, 0.f, 0.f), u1 = u0;
+      if (has_ad) {
+        u0 = *reinterpret_cast<const float4*>(sV + wave * VP + 8 * c);
+        u1 = *reinterpret_cast<const float4*>(sV + wave * VP + 8 * c + 4);
+      }
+      const float up[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[j][e] = up[e] + zz[e] + r8[e];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[j][e] = 0.f;
+    }
   }
-  if (a.norm == Norm::None) {
+  auto store_rows = [&](bf16* dst, const float (*val)[8]) {
 #pragma unroll
-    for (int j = 0; j < FB; ++j) St<bf16>::st4(static_cast<bf16*>(a.out), wrow + 4 * lane + 256 * j, v[j]);
+    for (int j = 0; j < NJ; ++j) {
+      const int c = lane + 64 * j;
+      if (NC % 64 == 0 || c < NC) st16(dst + wrow + 8 * c, pack_frag(val[j]), nt);
+    }
+  };
+  if (a.norm == Norm::None) {
+    store_rows(static_cast<bf16*>(a.out), v);
     return;
   }
   constexpr float inv_d = 1.f / (float)D;
@@ -167,40 +195,38 @@ __global__ __launch_bounds__(1024) void adapter_fwd_rows(AdapterFwdArgs a) {
   if (a.norm == Norm::LN) {
     float s = 0.f;
 #pragma unroll
-    for (int j = 0; j < FB; ++j) s += (v[j][0] + v[j][1]) + (v[j][2] + v[j][3]);
+    for (int j = 0; j < NJ; ++j)
+      s += ((v[j][0] + v[j][1]) + (v[j][2] + v[j][3])) + ((v[j][4] + v[j][5]) + (v[j][6] + v[j][7]));
     mean = wave_sum(s) * inv_d;
   } else {
-#pragma unroll
-    for (int j = 0; j < FB; ++j)  // RMS: the residual stream h itself is an output
-      St<bf16>::st4(static_cast<bf16*>(a.out), wrow + 4 * lane + 256 * j, v[j]);
+    store_rows(static_cast<bf16*>(a.out), v);  // RMS: the residual stream h itself is an output
   }
   float s2 = 0.f;
 #pragma unroll
-  for (int j = 0; j < FB; ++j)
+  for (int j = 0; j < NJ; ++j)
+    if (NC % 64 == 0 || lane + 64 * j < NC)
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const float c = v[j][q] - mean;
-      s2 += c * c;
-    }
+      for (int e = 0; e < 8; ++e) {
+        const float c = v[j][e] - mean;
+        s2 += c * c;
+      }
   const float rstd = rsqrtf(wave_sum(s2) * inv_d + a.eps);
   if (a.rstd && lane == 0) a.rstd[tw] = rstd;
-  bf16* out = static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm);
+  float xh[NJ][8], o[NJ][8];
 #pragma unroll
-  for (int j = 0; j < FB; ++j) {
-    const int f = 4 * lane + 256 * j;
-    float xh[4], o[4];
-    const float gm[4] = {__uint_as_float(gmv[j].x << 16), __uint_as_float(gmv[j].x & 0xffff0000u),
-                         __uint_as_float(gmv[j].y << 16), __uint_as_float(gmv[j].y & 0xffff0000u)};
-    const uint2 bq = a.norm == Norm::LN ? btv[j] : make_uint2(0, 0);  // RMSNorm has no shift
-    const float bt[4] = {__uint_as_float(bq.x << 16), __uint_as_float(bq.x & 0xffff0000u),
-                         __uint_as_float(bq.y << 16), __uint_as_float(bq.y & 0xffff0000u)};
+  for (int j = 0; j < NJ; ++j) {
+    const int c = min(lane + 64 * j, NC - 1);  // lanes past the row compute and store nothing useful
+    float gm[8], bt[8];
+    unpack_frag(*reinterpret_cast<const bf16x8*>(sGB + 8 * c), gm);
+    unpack_frag(*reinterpret_cast<const bf16x8*>(sGB + D + 8 * c), bt);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) xh[q] = (v[j][q] - mean) * rstd;
-#pragma unroll
-    for (int q = 0; q < 4; ++q) o[q] = xh[q] * gm[q] + bt[q];
-    St<bf16>::st4(out, wrow + f, o);
-    if (a.xhat) St<bf16>::st4(static_cast<bf16*>(a.xhat), wrow + f, xh);
+    for (int e = 0; e < 8; ++e) {
+      xh[j][e] = (v[j][e] - mean) * rstd;
+      o[j][e] = xh[j][e] * gm[e] + (a.norm == Norm::LN ? bt[e] : 0.f);  // RMSNorm has no shift
+    }
   }
+  store_rows(static_cast<bf16*>(a.norm == Norm::LN ? a.out : a.out_norm), o);
+  if (a.xhat) store_rows(static_cast<bf16*>(a.xhat), xh);
 }
 
 // ================================================================ bf16 backward, d <= 1024
@@ -228,6 +254,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
   float* sV = sPart + KS * MB * TOKP;                              // [TOK][VP]
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, l16 = lane & 15, grp = lane >> 4;
   const int T = a.T;
+  const bool nt = stream_out((long)T * D * 2);  // outputs streamed (common.h)
   const int tw = xcd_block(blockIdx.x, gridDim.x) * TOK + wave;  // this wave's token in the row phases
   const bool twv = tw < T;
   const long wrow = (long)(twv ? tw : 0) * D;
@@ -322,7 +349,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
 #pragma unroll
   for (int j = 0; j < FB; ++j) {
     const int f = 4 * lane + 256 * j;
-    if (twv && a.dz) St<bf16>::st4(static_cast<bf16*>(a.dz), wrow + f, dz[j]);
+    if (twv && a.dz) St<bf16>::st4s(static_cast<bf16*>(a.dz), wrow + f, dz[j], nt);
     St<bf16>::st4(sdZ, (long)wave * DP + f, dz[j]);
   }
   if (!has_ad) return;
@@ -352,8 +379,8 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     const ErfGauss eg = erf_gauss_as(uf);
     const float phi2 = 1.f + eg.erf_z;
     const bf16 du = f2bf(sum * fmaf(uf * 0.39894228040143268f, eg.gauss, 0.5f * phi2));
-    if (twv) static_cast<bf16*>(a.du)[(long)tw * MB + unit] = du;
-    if (a.gu && twv) static_cast<bf16*>(a.gu)[(long)tw * MB + unit] = f2bf(0.5f * uf * phi2);
+    if (twv) St<bf16>::st_nt(static_cast<bf16*>(a.du), (long)tw * MB + unit, bf2f(du));
+    if (a.gu && twv) St<bf16>::st_nt(static_cast<bf16*>(a.gu), (long)tw * MB + unit, 0.5f * uf * phi2);
     sdU[wave * GP + unit] = du;
   }
   if (!a.dzin) return;
@@ -377,7 +404,7 @@ __global__ __launch_bounds__(NW * 64) void adapter_bwd_bf16(AdapterBwdArgs a) {
     const int f = 4 * lane + 256 * j;
     const float4 v = *reinterpret_cast<const float4*>(sV + wave * VP + f);
     const float o[4] = {dz[j][0] + v.x, dz[j][1] + v.y, dz[j][2] + v.z, dz[j][3] + v.w};
-    St<bf16>::st4(static_cast<bf16*>(a.dzin), wrow + f, o);
+    St<bf16>::st4s(static_cast<bf16*>(a.dzin), wrow + f, o, nt);
   }
 }
 
@@ -563,7 +590,8 @@ __global__ __launch_bounds__(256) void adapter_wide_down(const bf16* X, const bf
   for (int i = threadIdx.x; i < TOK * MB; i += 256) {
     const int tok = i / MB, j = i % MB;
     if (t0 + tok < T)
-      P[((long)kc * T + t0 + tok) * MB + j] = (red[0][j][tok] + red[1][j][tok]) + (red[2][j][tok] + red[3][j][tok]);
+      St<float>::st_nt(P, ((long)kc * T + t0 + tok) * MB + j,
+                       (red[0][j][tok] + red[1][j][tok]) + (red[2][j][tok] + red[3][j][tok]));
   }
 }
 
@@ -625,10 +653,10 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
     if (t < T) {
       if constexpr (BWD) {
         g = sum * gelu_grad_fast(bf2f(uiv[it]));
-        if (fc == 0) uo[(long)t * MB + j] = f2bf(g);
+        if (fc == 0) St<bf16>::st_nt(uo, (long)t * MB + j, g);
       } else {
         g = gelu_fast(sum);
-        if (fc == 0 && uo) uo[(long)t * MB + j] = f2bf(sum);
+        if (fc == 0 && uo) St<bf16>::st_nt(uo, (long)t * MB + j, sum);
       }
     }
     sG[tok * GP + j] = f2bf(g);
@@ -657,7 +685,7 @@ __global__ __launch_bounds__(256) void adapter_wide_up(const float* P, int nkc, 
     const float v[8] = {lo.x, lo.y, lo.z, lo.w, hi.x, hi.y, hi.z, hi.w};
 #pragma unroll
     for (int q = 0; q < 8; ++q) o[q] = v[q] + zf[q] + (R ? rf[q] : 0.f);
-    *reinterpret_cast<bf16x8*>(out + (long)(t0 + tok) * d + fc * WIDE_UC + f8) = pack_frag(o);
+    st16(out + (long)(t0 + tok) * d + fc * WIDE_UC + f8, pack_frag(o), stream_out((long)T * d * 2));
   }
 }
 
@@ -815,7 +843,7 @@ template <int FB>
 static hipError_t fwd_rows_k(const AdapterFwdArgs& a, hipStream_t s) {
   constexpr int D = 256 * FB;
   const size_t sh = (size_t)TOK * (D + 8) * 2 + (size_t)TOK * GP * 2 + (size_t)4 * MB * (TOK + 1) * 4 +
-                    (size_t)TOK * (D + 4) * 4;
+                    (size_t)TOK * (D + 4) * 4 + (size_t)TOK * D * 2 + (size_t)2 * D * 2;
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&adapter_fwd_rows<FB>),
@@ -904,6 +932,10 @@ hipError_t launch_adapter_fwd(int dtype, const AdapterFwdArgs& a, hipStream_t s)
   if (dtype == DT_BF16) {
     int nw, fb;
     if (!bf16_shape(a.d, nw, fb) || a.m != MB || !al16(a.z) || (a.wdn_t && (!al16(a.wdn_t) || !al16(a.wup_t))))
+      return hipErrorInvalidValue;
+    // the row kernels move 16 B per lane in every row and through the gain and shift
+    if (!al16(a.res) || !al16(a.out) || (a.out_norm && !al16(a.out_norm)) || (a.xhat && !al16(a.xhat)) ||
+        (a.gamma && !al16(a.gamma)) || (a.beta && !al16(a.beta)))
       return hipErrorInvalidValue;
     switch (fb) {  // d = 256, 512, 768, 1024, 2048, 3072, 4096
       case 1: return fwd_rows_k<1>(a, s);

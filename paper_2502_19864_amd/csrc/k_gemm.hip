@@ -54,8 +54,8 @@ __device__ __forceinline__ void epilogue4_f32(const GemmArgs& a, int m, int n, f
 __device__ __forceinline__ void ld8(const bf16* p, float v[8]) {
   unpack_frag(*reinterpret_cast<const bf16x8*>(p), v);
 }
-__device__ __forceinline__ void st8(bf16* p, const float v[8]) {
-  *reinterpret_cast<bf16x8*>(p) = pack_frag(v);
+__device__ __forceinline__ void st8(bf16* p, const float v[8], bool nt) {
+  st16(p, pack_frag(v), nt);
 }
 
 // bf16 epilogue on eight consecutive output columns n..n+7 of row m; the
@@ -73,23 +73,23 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float
       v[4] += hi.x; v[5] += hi.y; v[6] += hi.z; v[7] += hi.w;
     }
     if constexpr (E == Epi::Gelu) {
-      if (a.out2) st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + n, v);
+      if (a.out2) st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + n, v, a.nt);
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = gelu_logistic(v[i]);
     }
-    st8(out + r * a.ldo + n, v);
+    st8(out + r * a.ldo + n, v, a.nt);
   } else if constexpr (E == Epi::Resid) {
     float x[8];
     unpack_frag(aux8[0], x);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] += x[i];
-    st8(out + r * a.ldo + n, v);
+    st8(out + r * a.ldo + n, v, a.nt);
   } else if constexpr (E == Epi::DGelu) {
     float x[8];
     unpack_frag(aux8[0], x);
 #pragma unroll
     for (int i = 0; i < 8; ++i) v[i] *= gelu_grad_fast(x[i]);
-    st8(out + r * a.ldo + n, v);
+    st8(out + r * a.ldo + n, v, a.nt);
   } else if constexpr (E == Epi::DSwiGlu) {
     float g[8], u[8], dg[8], du[8];
     unpack_frag(aux8[0], g);
@@ -100,8 +100,8 @@ __device__ __forceinline__ void epilogue8(const GemmArgs& a, int m, int n, float
       du[i] = v[i] * g[i] * sg;
       dg[i] = v[i] * u[i] * (sg + g[i] * sg * (1.f - sg));
     }
-    st8(out + r * a.ldo + n, dg);
-    st8(out + r * a.ldo + a.half + n, du);
+    st8(out + r * a.ldo + n, dg, a.nt);
+    st8(out + r * a.ldo + a.half + n, du, a.nt);
   }
 }
 
@@ -112,10 +112,10 @@ __device__ __forceinline__ void epilogue_swiglu8(const GemmArgs& a, int m, int f
   float o[8];
 #pragma unroll
   for (int i = 0; i < 8; ++i) o[i] = g[i] * sigmoid_f(g[i]) * u[i];
-  st8(static_cast<bf16*>(a.out) + r * a.ldo + f, o);
+  st8(static_cast<bf16*>(a.out) + r * a.ldo + f, o, a.nt);
   if (a.out2) {
-    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + f, g);
-    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + a.half + f, u);
+    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + f, g, a.nt);
+    st8(static_cast<bf16*>(a.out2) + r * a.ldo2 + a.half + f, u, a.nt);
   }
 }
 
@@ -396,8 +396,8 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
 #pragma unroll 4
       for (int idx = tid; idx < BM * CPRA; idx += NT) {
         const int row = idx / CPRA, q = idx % CPRA, part = q / (DHA / 8), c = (q % (DHA / 8)) * 8;
-        *reinterpret_cast<bf16x8*>(static_cast<bf16*>(a.out) + (long)(m0 + row) * a.ldo + n0 + part * DHA + c) =
-            *reinterpret_cast<const bf16x8*>(sT + part * TILE + row * TPA + c);
+        st16(static_cast<bf16*>(a.out) + (long)(m0 + row) * a.ldo + n0 + part * DHA + c,
+             *reinterpret_cast<const bf16x8*>(sT + part * TILE + row * TPA + c), a.nt);
       }
     }
     const int h = n0 / BN, H = N / BN, seq = m0 / BM;
@@ -484,8 +484,8 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
           }
         }
         bf16* out = static_cast<bf16*>(a.out);
-        st8(out + (long)m * a.ldo + n1, v1);
-        st8(out + (long)m * a.ldo + n2, v2);
+        st8(out + (long)m * a.ldo + n1, v1, a.nt);
+        st8(out + (long)m * a.ldo + n2, v2, a.nt);
       }
     } else if constexpr (HAS_AUX) {
       static_assert(NCH8 % NT == 0, "whole passes");
@@ -716,7 +716,12 @@ static hipError_t launch_epi(Epi e, Cfg cfg, int dtype, const GemmArgs& a, hipSt
 static bool al16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
 static bool al8(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 7u) == 0; }
 
-hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a, hipStream_t s) {
+hipError_t launch_gemm(int dtype, Role role, Epi epi, const GemmArgs& a_in, hipStream_t s) {
+  GemmArgs a = a_in;
+  {  // stream the outputs when the largest tensor written is small enough (common.h)
+    const long esz = dtype == DT_BF16 ? 2 : 4;
+    a.nt = (long)a.M * a.N * esz * (epi == Epi::DSwiGlu ? 2 : 1) <= NT_MAX_BYTES;
+  }
   if (epi == Epi::Attn) {
     // bf16 QKV projection, one head (d_head 64) of one 128-token sequence per
     // 128x192 tile; 16-B rows everywhere, 32-bit operand byte offsets

@@ -36,7 +36,7 @@ __device__ __forceinline__ float block_sum256(float v, float* red) {
   return t;
 }
 __device__ __forceinline__ void ld8f(const bf16* p, float v[8]) { unpack_frag(ld_frag(p), v); }
-__device__ __forceinline__ void st8f(bf16* p, const float v[8]) { *reinterpret_cast<bf16x8*>(p) = pack_frag(v); }
+__device__ __forceinline__ void st8f(bf16* p, const float v[8], bool nt) { st16(p, pack_frag(v), nt); }
 
 // h = x1 (+ x2); LN: out = LN(h) g + b (out may alias x1); RMS: out = h (when
 // x2 is given) and out_norm = RMSNorm(h) g; None: out = h.  xhat, rstd stashed
@@ -47,6 +47,7 @@ __global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm
   __shared__ float red[4];
   const long row = (long)blockIdx.x * d;
   const int nc = d / 8;
+  const bool nt = stream_out((long)gridDim.x * d * 2);  // one row per workgroup
   // every load up front, none conditional on a lane or an operand: a chunk past the row
   // reads chunk 0, an absent operand reads x1 (gamma) instead, masked afterwards; so no
   // load waits for the one before it
@@ -76,7 +77,7 @@ __global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm
 #pragma unroll
     for (int i = 0; i < NORM_NPT; ++i) {
       const int c = threadIdx.x + 256 * i;
-      if (c < nc) st8f(out + row + 8 * c, v[i]);
+      if (c < nc) st8f(out + row + 8 * c, v[i], nt);
     }
     if (norm == Norm::None) return;
   }
@@ -114,8 +115,8 @@ __global__ __launch_bounds__(256) void norm_rows_fwd_bf16(int d, float eps, Norm
       xh[q] = (v[i][q] - mean) * rs;
       o[q] = xh[q] * g[q] + (norm == Norm::LN ? b[q] : 0.f);
     }
-    st8f(dst + row + 8 * c, o);
-    if (xhat) st8f(xhat + row + 8 * c, xh);
+    st8f(dst + row + 8 * c, o, nt);
+    if (xhat) st8f(xhat + row + 8 * c, xh, nt);
   }
 }
 
@@ -126,6 +127,7 @@ __global__ __launch_bounds__(256) void norm_rows_bwd_bf16(int d, Norm norm, cons
   __shared__ float red[4];
   const long row = (long)blockIdx.x * d;
   const int nc = d / 8;
+  const bool nt = stream_out((long)gridDim.x * d * 2);
   float gg[NORM_NPT][8], xh[NORM_NPT][8];
   float s1 = 0.f, s2 = 0.f;
 #pragma unroll
@@ -153,7 +155,7 @@ __global__ __launch_bounds__(256) void norm_rows_bwd_bf16(int d, Norm norm, cons
     if (norm == Norm::RMS) ld8f(dres + row + 8 * c, r);
 #pragma unroll
     for (int q = 0; q < 8; ++q) o[q] = r[q] + rs * (gg[i][q] - m1 - xh[i][q] * m2);
-    st8f(dz + row + 8 * c, o);
+    st8f(dz + row + 8 * c, o, nt);
   }
 }
 
@@ -389,6 +391,7 @@ __global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, i
   // the two-class instantiation runs only with C == 2: a compile-time class count leaves
   // no class guard around a load, so the loads of a row go out together
   const int C = CN == 2 ? 2 : C_;
+  const bool nt = stream_out((long)B * S * d * (long)sizeof(T));  // dY streamed (common.h)
   if (blockIdx.x > 0) {
     const int nz = gridDim.x - 1, z = blockIdx.x - 1;
     const int vpr = d * (int)sizeof(T) / 16;  // 16-B vectors per row
@@ -396,7 +399,7 @@ __global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, i
     for (long v = (long)z * HEAD_NT + threadIdx.x; v < nvec; v += (long)nz * HEAD_NT) {
       const long rr = v / vpr;
       const long r = (rr / (S - 1)) * S + 1 + rr % (S - 1);
-      reinterpret_cast<uint4*>(dy + r * d)[v % vpr] = make_uint4(0, 0, 0, 0);
+      st16(reinterpret_cast<uint4*>(dy + r * d) + v % vpr, zero_frag(), nt);
     }
     return;
   }
@@ -512,7 +515,7 @@ __global__ __launch_bounds__(HEAD_NT) void head_ce_k(const T* y, int B, int S, i
                 gacc[c] += yv[u] * sdl[sm][c];
                 g += sdl[sm][c] * wv[c];
               }
-            St<T>::st(dy, (long)(b0 + sm) * S * d + i, g);
+            St<T>::st_nt(dy, (long)(b0 + sm) * S * d + i, g);
           }
         }
       if (fb == 0) {  // the bias gradient and the loss, once

@@ -63,6 +63,7 @@ struct GemmArgs {
   // Rope only: (cos, sin) of pos * theta^(-2i/dh), [positions][rope_dh / 2]
   const float2* rope_tab;
   int rope_S, rope_dh, rope_cols;
+  int nt;  // set by launch_gemm: outputs stored with the non-temporal hint
 };
 
 // Names of the GEMM call sites (each gets its own kernel symbol).

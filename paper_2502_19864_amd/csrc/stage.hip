@@ -395,6 +395,9 @@ extern "C" ringada_status ringada_stage_bind_block(ringada_stage* st, int32_t bl
     return fail(RINGADA_E_INVALID, "missing frozen weight");
   const bool has_post = w->b_qkv && w->b_o && w->norm1_b && w->b_in && w->b_out && w->norm2_b;
   const bool any_post = w->b_qkv || w->b_o || w->norm1_b || w->b_in || w->b_out || w->norm2_b;
+  for (const void* q : {w->norm1_g, w->norm1_b, w->norm2_g, w->norm2_b})
+    if (reinterpret_cast<uintptr_t>(q) & 15u)
+      return fail(RINGADA_E_INVALID, "norm gains and shifts must be 16-byte aligned");
   if (post && !has_post) return fail(RINGADA_E_INVALID, "post-LN block needs every bias and beta");
   if (!post && any_post) return fail(RINGADA_E_INVALID, "pre-RMS block takes no bias or beta");
   for (const ringada_adapter* a : {attn, ffn}) {

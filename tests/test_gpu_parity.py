@@ -434,6 +434,16 @@ def test_state_machine_and_workspace_errors(torch):
         with pytest.raises(B.RingadaError) as e:
             st.backward(dy, w.n_blocks)
         assert e.value.status == B.RINGADA_E_STATE
+        # the norm gains and shifts must be 16-byte aligned (the row kernels
+        # move 16 B per lane); refused before anything is bound
+        bad = {k: v.data_ptr() for k, v in st.frozen[0].items()}
+        bad["norm1_g"] += 2
+        ca = [B.Adapter(**{k: v.data_ptr() for k, v in t.items()}) for t in st.adapters[0]]
+        with pytest.raises(B.RingadaError) as e:
+            B.ringada_stage_bind_block(st.handle, 0, B.BlockWeights(**bad), ca[0], ca[1], st.block_mem[0],
+                                       st.block_bytes, st.sptr)
+        assert e.value.status == B.RINGADA_E_INVALID
+        st.forward(x, y, w.n_blocks)  # the stage is unchanged
         torch.cuda.synchronize()
     finally:
         st.close()
