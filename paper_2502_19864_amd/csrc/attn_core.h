@@ -69,14 +69,41 @@ __device__ __forceinline__ void store_rows(f32x16 (&acc)[DH / 32], float scale, 
     }
 }
 
+// The same rows (unscaled, not rotated) through LDS: each lane writes its row
+// into the 32 staging rows (pitch DH + 8, private to the wave), then each
+// store instruction writes whole rows, 16 B per lane (8 rows of 128 B at DH
+// 64), so the stores can be streamed (st16).  One wave's LDS operations run in
+// order, so the reads see the writes without a barrier.
+template <int DH>
+__device__ __forceinline__ void store_rows_staged(const f32x16 (&acc)[DH / 32], float scale, int half, int lane,
+                                                  bf16* stage, bf16* dst0, long ld, bool nt) {
+  const int l32 = lane & 31;
+#pragma unroll
+  for (int db = 0; db < DH / 32; ++db)
+#pragma unroll
+    for (int g = 0; g < 4; ++g) {
+      float v[4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) v[q] = acc[db][4 * g + q] * scale;
+      St<bf16>::st4(stage + l32 * (DH + 8), db * 32 + 8 * g + 4 * half, v);
+    }
+  constexpr int CPR = DH / 8;  // 16-B chunks per row
+#pragma unroll
+  for (int k = lane; k < 32 * CPR; k += 64) {
+    const int row = k / CPR, c = k % CPR;
+    st16(dst0 + row * ld + 8 * c, ld_frag(stage + row * (DH + 8) + 8 * c), nt);
+  }
+}
+
 // One wave's 32 queries q0..q0+31 against a whole sequence of KT = 128 keys,
 // all staged in LDS as row-major [row][dim] bf16 tiles of pitch DH + 8 (no
-// mask: every key is valid).  Writes the wave's O rows (bf16, each lane its
-// query's row at o_row) and, from lanes 0..31, the base-2 log-sum-exp of the
-// scaled scores at lse_row[query].
+// mask: every key is valid).  Writes the wave's O rows (bf16, rows of stride
+// ld_o from o0, the row of query q0) and, from lanes 0..31, the base-2
+// log-sum-exp of the scaled scores at lse_row[query].  The wave's own Q rows
+// are read once, first, and then hold the O tile on its way out.
 template <int DH>
-__device__ __forceinline__ void attn_seq128_wave(const bf16* sQ, const bf16* sK, const bf16* sV, int q0, int lane,
-                                                 bf16* o_row, float* lse_row) {
+__device__ __forceinline__ void attn_seq128_wave(bf16* sQ, const bf16* sK, const bf16* sV, int q0, int lane,
+                                                 bf16* o0, long ld_o, bool nt, float* lse_row) {
   const int half = lane >> 5, l32 = lane & 31, q = q0 + l32;
   const float sl2 = kLog2e * rsqrtf((float)DH);
   bf16x8 qf[DH / 16];
@@ -120,7 +147,7 @@ __device__ __forceinline__ void attn_seq128_wave(const bf16* sQ, const bf16* sK,
 #pragma unroll
       for (int db = 0; db < DH / 32; ++db) oacc[db] = mfma32(perm_frag<DH>(sV, db, kb, j, lane), pf, oacc[db]);
     }
-  store_rows<DH>(oacc, 1.f / rs, false, q, nullptr, half, o_row);
+  store_rows_staged<DH>(oacc, 1.f / rs, half, lane, sQ + q0 * (DH + 8), o0, ld_o, nt);
   if (half == 0) lse_row[q] = m2 + log2f(rs);
 }
 

@@ -399,10 +399,12 @@ __device__ __forceinline__ void gemm_bf16_pipe_body(const GemmArgs& a) {
         st16(static_cast<bf16*>(a.out) + (long)(m0 + row) * a.ldo + n0 + part * DHA + c,
              *reinterpret_cast<const bf16x8*>(sT + part * TILE + row * TPA + c), a.nt);
       }
+      barrier();  // every wave's Q rows are read here; each wave then reuses its own for O
     }
     const int h = n0 / BN, H = N / BN, seq = m0 / BM;
-    bf16* orow = static_cast<bf16*>(a.out2) + (long)(m0 + wave * 32 + l32) * a.ldo2 + h * DHA;
-    attn_seq128_wave<DHA>(sT, sT + TILE, sT + 2 * TILE, wave * 32, lane, orow, a.lse + (long)(seq * H + h) * BM);
+    bf16* o0 = static_cast<bf16*>(a.out2) + (long)(m0 + wave * 32) * a.ldo2 + h * DHA;
+    attn_seq128_wave<DHA>(sT, sT + TILE, sT + 2 * TILE, wave * 32, lane, o0, a.ldo2, a.nt,
+                          a.lse + (long)(seq * H + h) * BM);
     return;
   }
   auto ld_tile8 = [&](int row, int col, float v[8]) {
