@@ -7,7 +7,10 @@ epilogue (pipelined 128x192, 128x96, 128x128 with two or three stages,
 round of 256x128 tiles onto 128x128).  The stage workloads of the other
 tests reach about half of the legal (role, epilogue, tile) combinations.
 The one-block stages below reach every other one (each entry lists what it
-adds), at token counts up to 32768.
+adds), at token counts up to 32768.  Outputs of at most 32 MiB are stored
+with the non-temporal hint, larger ones plainly: the 32768-token d = 1024
+case runs the plain arm of the projection GEMMs, the fused attention and the
+adapter rows.
 
 Every op of a block is per sequence, so each case runs the whole batch on
 the GPU and compares three sequences with the oracle: the first, the middle
@@ -69,6 +72,9 @@ TILES = {
     "tiles_llama_d768_b8": _w("tiles_llama_d768_b8", "llama", 768, 12, 64, 128, 8, 2108),
     # 256x128 QKV (store) of the post-LN block: 256x192 would leave CUs idle
     "tiles_bert_d3072_b4": _w("tiles_bert_d3072_b4", "bert", 3072, 48, 64, 256, 4, 2109),
+    # outputs past the 32 MiB streaming bound (plain stores): the adapter and norm rows
+    # (64 MiB), the QKV projection with the fused attention (192 MiB) and its O rows
+    "tiles_bert_d1024_t32k": _w("tiles_bert_d1024_t32k", "bert", 1024, 16, 64, 128, 256, 2110),
 }
 
 
