@@ -24,17 +24,14 @@ constexpr int GP = MB + 8;
 // ================================================================ bf16 forward, d <= 1024
 // One workgroup of 16 waves per 16 tokens: the whole adapter, the residual
 // add and the norm in one kernel.
-// Laid out so that nothing waits twice on memory and every global access
-// moves 16 B per lane: all global loads are issued before the first barrier
-// (the norm's gain and shift once per workgroup, the residual and z tiles by
-// DMA into LDS, the weight fragments of both projections into registers); the
-// up projection's fp32 result is staged in LDS; the add + norm phase then
-// runs one wave per token (NW == TOK), so the row statistics are wave
-// reductions, and each lane handles the 8 features of chunks lane + 64 j.
-// The memory pipe of a CU takes about as long per wave instruction whatever
-// its width, so the 16-B accesses (with the gain and shift loaded once, not
-// by every wave) cut this kernel's load and store instructions by a third.
-// The down projection's k-slice
+// Laid out so that nothing waits twice on memory and every row access moves
+// 16 B per lane: all global loads are issued before the first barrier (the
+// norm's gain and shift once per workgroup, the residual and z tiles by DMA
+// into LDS, the weight fragments of both projections into registers); the up
+// projection's fp32 result is staged in LDS; the add + norm phase then runs
+// one wave per token (NW == TOK), so the row statistics are wave reductions,
+// and each lane handles the 8 features of chunks lane + 64 j.  The outputs are
+// streamed (st16).  The down projection's k-slice
 // partial sums go through LDS unit-major, [slice][unit][token] with a token
 // stride of 17 floats: the MFMA writes (16 tokens of 4 units per lane group)
 // and the GELU phase's reads (one unit per lane) spread over the banks,
